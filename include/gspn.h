@@ -1,0 +1,137 @@
+/*
+ * gspn.h -- C ABI of the GSPN 2D line-scan propagation on AMD Instinct MI355X (gfx950).
+ *
+ * The operation (Generalized Spatial Propagation Network, Sec. 3.1 Eq. 1-2,
+ * Sec. 3.3; supplementary Eq. 7-9):
+ *
+ *   For each (b, c) plane of an H x W map and each direction d of `mask`,
+ *   lines (rows for T2B/B2T, columns for L2R/R2L) are visited in the
+ *   direction's order.  With the state before the first line equal to zero,
+ *
+ *     h_d[line][p] = sum_{k=0..2} w_{d,k}[line][p] * h_d[prev line][p + k - 1]
+ *                    + lam[line][p] * x[line][p]
+ *
+ *   where p is the position along the line and a neighbour outside the line
+ *   contributes 0.  The output merges the directions by summation:
+ *
+ *     y = u * sum_d h_d
+ *
+ *   Neighbours (k = 0, 1, 2 is offset -1, 0, +1 along the line coordinate):
+ *     T2B  rows 0..H-1   (i-1, j-1) (i-1, j) (i-1, j+1)
+ *     B2T  rows H-1..0   (i+1, j-1) (i+1, j) (i+1, j+1)
+ *     L2R  cols 0..W-1   (i-1, j-1) (i, j-1) (i+1, j-1)   (the case of Alg. 1)
+ *     R2L  cols W-1..0   (i-1, j+1) (i, j+1) (i+1, j+1)
+ *
+ *   The backward (Alg. 2) is the exact adjoint for the loss <dy, y>.
+ *
+ * Layouts (all tensors contiguous, element type `dtype`):
+ *   x, lam, u, y, dy, dx, dlam, du : (B, C, H, W)
+ *   w, dw                          : (n, 3, B, C, H, W), n = popcount(mask), the
+ *                                    directions in increasing bit order; w[d][k] is
+ *                                    the weight the RECEIVING pixel gives its
+ *                                    neighbour k, stored at that pixel's (i, j).
+ *   lam and u are shared by all directions.
+ *
+ * Arithmetic: inputs are widened to fp32, every sum and product is fp32, and
+ * each output element is rounded once (round-to-nearest-even for bf16).
+ *
+ * Ownership: every data pointer is device memory owned by the caller.  The
+ * library allocates nothing; scratch memory is passed in as `workspace`
+ * (size from the matching *_workspace_bytes call, 256-byte aligned).  No state
+ * is kept between calls, so calls on different streams are independent.
+ *
+ * Empty problems: if B, C, H or W is 0 there is nothing to compute; the call
+ * returns GSPN_OK after checking dtype, mask and algo, and pointers are not
+ * inspected.
+ *
+ * Errors: 0 on success, a positive GSPN_ERR_* otherwise.  Arguments are
+ * checked on the host before anything is launched; on an error nothing is
+ * written.  Launch failures return GSPN_ERR_HIP.  Kernels run asynchronously
+ * on `stream` (a hipStream_t; NULL = the default stream), so a device fault
+ * surfaces at the caller's next synchronisation.
+ */
+#ifndef GSPN_H
+#define GSPN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { GSPN_F32 = 0, GSPN_BF16 = 1 } gspn_dtype;
+
+enum {
+  GSPN_DIR_T2B = 1u, /* top to bottom */
+  GSPN_DIR_B2T = 2u, /* bottom to top */
+  GSPN_DIR_L2R = 4u, /* left to right */
+  GSPN_DIR_R2L = 8u  /* right to left */
+};
+
+enum {
+  GSPN_OK = 0,
+  GSPN_ERR_NULL = 1,        /* a required pointer is NULL */
+  GSPN_ERR_SHAPE = 2,       /* a dimension < 0, or an element count overflows int64 */
+  GSPN_ERR_MASK = 3,        /* mask is 0 or has bits above bit 3 */
+  GSPN_ERR_DTYPE = 4,       /* unknown dtype */
+  GSPN_ERR_ALIGN = 5,       /* a pointer is not aligned to its element size (workspace: 256 B) */
+  GSPN_ERR_ALIAS = 6,       /* an output overlaps an input or another output */
+  GSPN_ERR_UNSUPPORTED = 7, /* H or W above GSPN_MAX_LINE, or a forced algorithm that cannot run */
+  GSPN_ERR_WORKSPACE = 8,   /* workspace NULL or smaller than required */
+  GSPN_ERR_HIP = 9          /* a HIP launch or runtime call failed */
+};
+
+/* Longest line (H and W) the kernels accept. */
+#define GSPN_MAX_LINE 4096
+
+/* Algorithm selection (the `algo` argument).  AUTO picks the fastest kernel
+ * family for the shape; the others force one family (for testing), and
+ * return GSPN_ERR_UNSUPPORTED when it cannot take the shape. */
+enum {
+  GSPN_ALGO_AUTO = 0,
+  GSPN_ALGO_RESIDENT = 1, /* whole plane kept on chip, all directions in one kernel */
+  GSPN_ALGO_STREAM = 2    /* one pass per direction through an fp32 workspace */
+};
+
+/* Bytes of workspace gspn_scan_fwd needs for this problem (0 if none). */
+size_t gspn_scan_fwd_workspace_bytes(int64_t B, int64_t C, int64_t H, int64_t W,
+                                     uint32_t mask, int dtype, int algo);
+
+/*
+ * Forward scan (Eq. 1-2): y = u * sum_{d in mask} h_d.
+ *   x, w, lam, u : inputs (see layouts above); y : output, fully overwritten.
+ *   workspace    : device scratch of at least gspn_scan_fwd_workspace_bytes()
+ *                  bytes, may be NULL when that size is 0.
+ */
+int gspn_scan_fwd(const void* x, const void* w, const void* lam, const void* u, void* y,
+                  int64_t B, int64_t C, int64_t H, int64_t W, uint32_t mask, int dtype,
+                  int algo, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of workspace gspn_scan_bwd needs for this problem (0 if none). */
+size_t gspn_scan_bwd_workspace_bytes(int64_t B, int64_t C, int64_t H, int64_t W,
+                                     uint32_t mask, int dtype, int algo);
+
+/*
+ * Backward scan (Alg. 2, exact adjoint of Eq. 1-2) for the loss <dy, y>:
+ *   inputs dy, x, w, lam, u (same values as the forward call);
+ *   outputs dx, dlam, du (B, C, H, W) and dw (n, 3, B, C, H, W), fully
+ *   overwritten (not accumulated).  The forward state is recomputed inside,
+ *   so no tensor from the forward call is needed.
+ */
+int gspn_scan_bwd(const void* dy, const void* x, const void* w, const void* lam, const void* u,
+                  void* dx, void* dw, void* dlam, void* du,
+                  int64_t B, int64_t C, int64_t H, int64_t W, uint32_t mask, int dtype,
+                  int algo, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Static, NUL-terminated description of a status code. */
+const char* gspn_strerror(int status);
+
+/* Library version as 10000*major + 100*minor + patch. */
+int gspn_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GSPN_H */

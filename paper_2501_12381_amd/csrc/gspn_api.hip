@@ -1,0 +1,255 @@
+// C ABI of the GSPN line scan: argument checking, workspace sizing and dispatch.
+// Host code only; the kernels live in gspn_stream.hip and gspn_resident.hip.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdint>
+#include <vector>
+
+#include "../../include/gspn.h"
+#include "gspn_launch.hpp"
+
+using namespace gspn;
+
+namespace {
+
+constexpr size_t kWsAlign = 256;
+
+size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+int popcount4(uint32_t m) { return (int)((m & 1) + ((m >> 1) & 1) + ((m >> 2) & 1) + ((m >> 3) & 1)); }
+
+std::vector<int> dirs_of(uint32_t mask) {
+  std::vector<int> d;
+  for (int b : {DIR_T2B, DIR_B2T, DIR_L2R, DIR_R2L})
+    if (mask & (uint32_t)b) d.push_back(b);
+  return d;
+}
+
+size_t esize(int dtype) { return dtype == GSPN_F32 ? 4 : 2; }
+
+// checked a*b for non-negative int64
+bool mul_ok(int64_t a, int64_t b, int64_t* out) {
+  if (a == 0 || b == 0) { *out = 0; return true; }
+  if (a > INT64_MAX / b) return false;
+  *out = a * b;
+  return true;
+}
+
+struct Problem {
+  int64_t B, C, H, W, planes, npc;  // npc = elements per (B,C,H,W) tensor
+  int n;
+  bool empty;
+};
+
+int check_shape(int64_t B, int64_t C, int64_t H, int64_t W, uint32_t mask, int dtype, int algo,
+                Problem* p) {
+  if (dtype != GSPN_F32 && dtype != GSPN_BF16) return GSPN_ERR_DTYPE;
+  if (mask == 0 || mask > 15u) return GSPN_ERR_MASK;
+  if (algo < GSPN_ALGO_AUTO || algo > GSPN_ALGO_STREAM) return GSPN_ERR_UNSUPPORTED;
+  if (B < 0 || C < 0 || H < 0 || W < 0) return GSPN_ERR_SHAPE;
+  p->B = B; p->C = C; p->H = H; p->W = W;
+  p->n = popcount4(mask);
+  int64_t planes, plane, npc, wtot;
+  if (!mul_ok(B, C, &planes) || !mul_ok(H, W, &plane) || !mul_ok(planes, plane, &npc) ||
+      !mul_ok(npc, 3 * p->n, &wtot) || !mul_ok(wtot, 4, &wtot))
+    return GSPN_ERR_SHAPE;
+  p->planes = planes;
+  p->npc = npc;
+  p->empty = npc == 0;
+  if (p->empty) return GSPN_OK;
+  if (H > GSPN_MAX_LINE || W > GSPN_MAX_LINE) return GSPN_ERR_UNSUPPORTED;
+  if (planes > 0x7fffffffLL) return GSPN_ERR_UNSUPPORTED;
+  return GSPN_OK;
+}
+
+struct Range {
+  uintptr_t lo, hi;
+};
+bool overlap(Range a, Range b) { return a.lo < b.hi && b.lo < a.hi; }
+
+int check_ptrs(const std::vector<std::pair<const void*, size_t>>& ins,
+               const std::vector<std::pair<const void*, size_t>>& outs, size_t align) {
+  for (auto& p : ins)
+    if (!p.first) return GSPN_ERR_NULL;
+  for (auto& p : outs)
+    if (!p.first) return GSPN_ERR_NULL;
+  for (auto& p : ins)
+    if ((uintptr_t)p.first % align) return GSPN_ERR_ALIGN;
+  for (auto& p : outs)
+    if ((uintptr_t)p.first % align) return GSPN_ERR_ALIGN;
+  for (size_t i = 0; i < outs.size(); ++i) {
+    Range o{(uintptr_t)outs[i].first, (uintptr_t)outs[i].first + outs[i].second};
+    for (auto& p : ins)
+      if (overlap(o, Range{(uintptr_t)p.first, (uintptr_t)p.first + p.second})) return GSPN_ERR_ALIAS;
+    for (size_t j = i + 1; j < outs.size(); ++j)
+      if (overlap(o, Range{(uintptr_t)outs[j].first, (uintptr_t)outs[j].first + outs[j].second}))
+        return GSPN_ERR_ALIAS;
+  }
+  return GSPN_OK;
+}
+
+int check_ws(void* ws, size_t ws_bytes, size_t need,
+             const std::vector<std::pair<const void*, size_t>>& others) {
+  if (need == 0) return GSPN_OK;
+  if (!ws || ws_bytes < need) return GSPN_ERR_WORKSPACE;
+  if ((uintptr_t)ws % kWsAlign) return GSPN_ERR_ALIGN;
+  Range r{(uintptr_t)ws, (uintptr_t)ws + need};
+  for (auto& p : others)
+    if (p.first && overlap(r, Range{(uintptr_t)p.first, (uintptr_t)p.first + p.second}))
+      return GSPN_ERR_ALIAS;
+  return GSPN_OK;
+}
+
+bool resident_fits(const Problem& p, int dtype, bool backward);  // defined below
+
+int choose_algo(const Problem& p, int dtype, int algo, bool backward) {
+  if (algo == GSPN_ALGO_STREAM) return GSPN_ALGO_STREAM;
+  if (algo == GSPN_ALGO_RESIDENT) return resident_fits(p, dtype, backward) ? GSPN_ALGO_RESIDENT : -1;
+  return resident_fits(p, dtype, backward) ? GSPN_ALGO_RESIDENT : GSPN_ALGO_STREAM;
+}
+
+bool resident_fits(const Problem&, int, bool) { return false; }
+
+size_t fwd_ws_bytes(const Problem& p, int algo) {
+  if (algo == GSPN_ALGO_STREAM && p.n > 1) return round_up((size_t)p.npc * 4, kWsAlign);
+  return 0;
+}
+
+size_t bwd_ws_bytes(const Problem& p, int algo) {
+  if (algo == GSPN_ALGO_STREAM) return 3 * round_up((size_t)p.npc * 4, kWsAlign);
+  return 0;
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? GSPN_OK : GSPN_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+size_t gspn_scan_fwd_workspace_bytes(int64_t B, int64_t C, int64_t H, int64_t W, uint32_t mask,
+                                     int dtype, int algo) {
+  Problem p;
+  if (check_shape(B, C, H, W, mask, dtype, algo, &p) != GSPN_OK || p.empty) return 0;
+  const int a = choose_algo(p, dtype, algo, false);
+  return a < 0 ? 0 : fwd_ws_bytes(p, a);
+}
+
+size_t gspn_scan_bwd_workspace_bytes(int64_t B, int64_t C, int64_t H, int64_t W, uint32_t mask,
+                                     int dtype, int algo) {
+  Problem p;
+  if (check_shape(B, C, H, W, mask, dtype, algo, &p) != GSPN_OK || p.empty) return 0;
+  const int a = choose_algo(p, dtype, algo, true);
+  return a < 0 ? 0 : bwd_ws_bytes(p, a);
+}
+
+int gspn_scan_fwd(const void* x, const void* w, const void* lam, const void* u, void* y,
+                  int64_t B, int64_t C, int64_t H, int64_t W, uint32_t mask, int dtype, int algo,
+                  void* workspace, size_t workspace_bytes, void* stream) {
+  Problem p;
+  int st = check_shape(B, C, H, W, mask, dtype, algo, &p);
+  if (st != GSPN_OK || p.empty) return st;
+  const size_t es = esize(dtype);
+  const size_t tb = (size_t)p.npc * es, wb = tb * 3 * (size_t)p.n;
+  st = check_ptrs({{x, tb}, {w, wb}, {lam, tb}, {u, tb}}, {{y, tb}}, es);
+  if (st != GSPN_OK) return st;
+  const int a = choose_algo(p, dtype, algo, false);
+  if (a < 0) return GSPN_ERR_UNSUPPORTED;
+  const size_t need = fwd_ws_bytes(p, a);
+  st = check_ws(workspace, workspace_bytes, need, {{x, tb}, {w, wb}, {lam, tb}, {u, tb}, {y, tb}});
+  if (st != GSPN_OK) return st;
+
+  const std::vector<int> ds = dirs_of(mask);
+  const int n = (int)ds.size();
+  for (int i = 0; i < n; ++i) {
+    StreamFwdArgs s{};
+    s.x = x; s.lam = lam; s.u = u; s.y = y;
+    s.w = (const char*)w + (size_t)i * 3 * tb;
+    s.wstride = p.npc;
+    s.acc = n > 1 ? (float*)workspace : nullptr;
+    s.hprev_out = nullptr;
+    s.first = i == 0;
+    s.mode = (i == n - 1) ? MODE_FINAL : (i == 0 ? MODE_STORE : MODE_ADD);
+    s.planes = p.planes; s.H = (int)H; s.W = (int)W; s.dir = ds[i]; s.dtype = dtype;
+    s.stream = stream;
+    st = hip_status(stream_fwd_pass(s));
+    if (st != GSPN_OK) return st;
+  }
+  return GSPN_OK;
+}
+
+int gspn_scan_bwd(const void* dy, const void* x, const void* w, const void* lam, const void* u,
+                  void* dx, void* dw, void* dlam, void* du, int64_t B, int64_t C, int64_t H,
+                  int64_t W, uint32_t mask, int dtype, int algo, void* workspace,
+                  size_t workspace_bytes, void* stream) {
+  Problem p;
+  int st = check_shape(B, C, H, W, mask, dtype, algo, &p);
+  if (st != GSPN_OK || p.empty) return st;
+  const size_t es = esize(dtype);
+  const size_t tb = (size_t)p.npc * es, wb = tb * 3 * (size_t)p.n;
+  st = check_ptrs({{dy, tb}, {x, tb}, {w, wb}, {lam, tb}, {u, tb}},
+                  {{dx, tb}, {dw, wb}, {dlam, tb}, {du, tb}}, es);
+  if (st != GSPN_OK) return st;
+  const int a = choose_algo(p, dtype, algo, true);
+  if (a < 0) return GSPN_ERR_UNSUPPORTED;
+  const size_t need = bwd_ws_bytes(p, a);
+  st = check_ws(workspace, workspace_bytes, need,
+                {{dy, tb}, {x, tb}, {w, wb}, {lam, tb}, {u, tb}, {dx, tb}, {dw, wb}, {dlam, tb}, {du, tb}});
+  if (st != GSPN_OK) return st;
+
+  const size_t fb = round_up((size_t)p.npc * 4, kWsAlign);
+  float* hprev = (float*)workspace;
+  float* hsum = (float*)((char*)workspace + fb);
+  float* gsum = (float*)((char*)workspace + 2 * fb);
+  const std::vector<int> ds = dirs_of(mask);
+  for (int i = 0; i < (int)ds.size(); ++i) {
+    StreamFwdArgs f{};
+    f.x = x; f.lam = lam; f.u = nullptr; f.y = nullptr;
+    f.w = (const char*)w + (size_t)i * 3 * tb;
+    f.wstride = p.npc;
+    f.acc = hsum;
+    f.hprev_out = hprev;
+    f.first = i == 0;
+    f.mode = MODE_REC;
+    f.planes = p.planes; f.H = (int)H; f.W = (int)W; f.dir = ds[i]; f.dtype = dtype;
+    f.stream = stream;
+    st = hip_status(stream_fwd_pass(f));
+    if (st != GSPN_OK) return st;
+    StreamAdjArgs r{};
+    r.dy = dy; r.u = u;
+    r.w = f.w;
+    r.wstride = p.npc;
+    r.hprev = hprev;
+    r.dw = (char*)dw + (size_t)i * 3 * tb;
+    r.gsum = gsum;
+    r.first = i == 0;
+    r.planes = p.planes; r.H = (int)H; r.W = (int)W; r.dir = ds[i]; r.dtype = dtype;
+    r.stream = stream;
+    st = hip_status(stream_adj_pass(r));
+    if (st != GSPN_OK) return st;
+  }
+  GradFinishArgs g{};
+  g.x = x; g.lam = lam; g.dy = dy; g.gsum = gsum; g.hsum = hsum;
+  g.dx = dx; g.dlam = dlam; g.du = du; g.n = p.npc; g.dtype = dtype; g.stream = stream;
+  return hip_status(grad_finish(g));
+}
+
+const char* gspn_strerror(int status) {
+  switch (status) {
+    case GSPN_OK: return "success";
+    case GSPN_ERR_NULL: return "a required pointer is NULL";
+    case GSPN_ERR_SHAPE: return "invalid shape: negative dimension or element count overflow";
+    case GSPN_ERR_MASK: return "invalid direction mask: must be in [1, 15]";
+    case GSPN_ERR_DTYPE: return "unknown dtype";
+    case GSPN_ERR_ALIGN: return "misaligned pointer";
+    case GSPN_ERR_ALIAS: return "an output overlaps an input or another output";
+    case GSPN_ERR_UNSUPPORTED: return "unsupported: line longer than GSPN_MAX_LINE, too many planes, or forced algorithm cannot run";
+    case GSPN_ERR_WORKSPACE: return "workspace missing or too small";
+    case GSPN_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+int gspn_version(void) { return 100; }
+
+}  // extern "C"

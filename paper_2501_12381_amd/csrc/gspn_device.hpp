@@ -1,0 +1,105 @@
+// Device-side helpers shared by the GSPN kernels (gfx950 / CDNA4, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gspn {
+
+typedef __bf16 bf16;
+
+// ---------------------------------------------------------------------------
+// element conversion: inputs are widened to fp32, outputs rounded once
+// (bf16 stores use the hardware round-to-nearest-even convert).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float bf_lo(uint32_t v) { return __uint_as_float(v << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t v) { return __uint_as_float(v & 0xffff0000u); }
+__device__ __forceinline__ uint32_t pack_bf2(float a, float b) {
+  bf16 lo = (bf16)a, hi = (bf16)b;
+  return (uint32_t)__builtin_bit_cast(uint16_t, lo) | ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
+}
+
+__device__ __forceinline__ float to_f(float v) { return v; }
+__device__ __forceinline__ float to_f(bf16 v) { return (float)v; }
+template <typename T> __device__ __forceinline__ T from_f(float v);
+template <> __device__ __forceinline__ float from_f<float>(float v) { return v; }
+template <> __device__ __forceinline__ bf16 from_f<bf16>(float v) { return (bf16)v; }
+
+// Load N consecutive elements starting at p into fp32 registers.  The address
+// must be aligned to min(16, N * sizeof(T)) bytes.
+template <int N> __device__ __forceinline__ void ldv(const float* __restrict__ p, float* v) {
+  if constexpr (N == 1) {
+    v[0] = p[0];
+  } else if constexpr (N == 2) {
+    float2 t = *reinterpret_cast<const float2*>(p);
+    v[0] = t.x; v[1] = t.y;
+  } else {
+#pragma unroll
+    for (int q = 0; q < N; q += 4) {
+      float4 t = *reinterpret_cast<const float4*>(p + q);
+      v[q] = t.x; v[q + 1] = t.y; v[q + 2] = t.z; v[q + 3] = t.w;
+    }
+  }
+}
+template <int N> __device__ __forceinline__ void ldv(const bf16* __restrict__ p, float* v) {
+  if constexpr (N == 1) {
+    v[0] = (float)p[0];
+  } else if constexpr (N == 2) {
+    uint32_t t = *reinterpret_cast<const uint32_t*>(p);
+    v[0] = bf_lo(t); v[1] = bf_hi(t);
+  } else if constexpr (N == 4) {
+    uint2 t = *reinterpret_cast<const uint2*>(p);
+    v[0] = bf_lo(t.x); v[1] = bf_hi(t.x); v[2] = bf_lo(t.y); v[3] = bf_hi(t.y);
+  } else {
+#pragma unroll
+    for (int q = 0; q < N; q += 8) {
+      uint4 t = *reinterpret_cast<const uint4*>(p + q);
+      v[q] = bf_lo(t.x); v[q + 1] = bf_hi(t.x); v[q + 2] = bf_lo(t.y); v[q + 3] = bf_hi(t.y);
+      v[q + 4] = bf_lo(t.z); v[q + 5] = bf_hi(t.z); v[q + 6] = bf_lo(t.w); v[q + 7] = bf_hi(t.w);
+    }
+  }
+}
+
+// Store N consecutive elements (same alignment rule as ldv).
+template <int N> __device__ __forceinline__ void stv(float* __restrict__ p, const float* v) {
+  if constexpr (N == 1) {
+    p[0] = v[0];
+  } else if constexpr (N == 2) {
+    *reinterpret_cast<float2*>(p) = make_float2(v[0], v[1]);
+  } else {
+#pragma unroll
+    for (int q = 0; q < N; q += 4)
+      *reinterpret_cast<float4*>(p + q) = make_float4(v[q], v[q + 1], v[q + 2], v[q + 3]);
+  }
+}
+template <int N> __device__ __forceinline__ void stv(bf16* __restrict__ p, const float* v) {
+  if constexpr (N == 1) {
+    p[0] = (bf16)v[0];
+  } else if constexpr (N == 2) {
+    *reinterpret_cast<uint32_t*>(p) = pack_bf2(v[0], v[1]);
+  } else if constexpr (N == 4) {
+    *reinterpret_cast<uint2*>(p) = make_uint2(pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]));
+  } else {
+#pragma unroll
+    for (int q = 0; q < N; q += 8)
+      *reinterpret_cast<uint4*>(p + q) =
+          make_uint4(pack_bf2(v[q], v[q + 1]), pack_bf2(v[q + 2], v[q + 3]),
+                     pack_bf2(v[q + 4], v[q + 5]), pack_bf2(v[q + 6], v[q + 7]));
+  }
+}
+
+// ---------------------------------------------------------------------------
+// cross-lane moves inside a wave64 (DPP wave shifts; all 64 lanes must be active)
+// ---------------------------------------------------------------------------
+// lane l receives lane l-1's value; lane 0 receives 0
+__device__ __forceinline__ float from_prev_lane(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v),
+                                                               0x138 /* wave_shr:1 */, 0xf, 0xf, false));
+}
+// lane l receives lane l+1's value; lane 63 receives 0
+__device__ __forceinline__ float from_next_lane(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v),
+                                                               0x130 /* wave_shl:1 */, 0xf, 0xf, false));
+}
+
+}  // namespace gspn

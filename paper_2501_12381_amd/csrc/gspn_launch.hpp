@@ -1,0 +1,74 @@
+// Internal launch interface between the C ABI (gspn_api.cpp) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace gspn {
+
+enum { DIR_T2B = 1, DIR_B2T = 2, DIR_L2R = 4, DIR_R2L = 8 };
+enum { MODE_STORE = 0, MODE_ADD = 1, MODE_FINAL = 2, MODE_REC = 3 };
+constexpr int kMaxWaves = 16;
+
+// ---- streaming family: one pass per direction --------------------------------
+struct StreamFwdArgs {
+  const void* x;
+  const void* lam;
+  const void* w;      // this direction's w0 (w1, w2 follow at +wstride, +2*wstride)
+  int64_t wstride;    // elements between the three weight maps (B*C*H*W)
+  const void* u;      // MODE_FINAL only
+  float* acc;         // fp32 accumulator (MODE_REC: running sum of h)
+  void* y;            // MODE_FINAL only
+  float* hprev_out;   // MODE_REC only: h of the previous line, per line
+  int first;          // MODE_REC: first direction (store instead of add)
+  int mode;
+  int64_t planes;
+  int H, W, dir, dtype;
+  void* stream;
+};
+hipError_t stream_fwd_pass_f32(const StreamFwdArgs& a);
+hipError_t stream_fwd_pass_bf16(const StreamFwdArgs& a);
+inline hipError_t stream_fwd_pass(const StreamFwdArgs& a) {
+  return a.dtype == 0 ? stream_fwd_pass_f32(a) : stream_fwd_pass_bf16(a);
+}
+
+struct StreamAdjArgs {
+  const void* dy;
+  const void* u;
+  const void* w;
+  int64_t wstride;
+  const float* hprev;
+  void* dw;           // this direction's dw0 (dw1, dw2 at +wstride, +2*wstride)
+  float* gsum;
+  int first;
+  int64_t planes;
+  int H, W, dir, dtype;
+  void* stream;
+};
+hipError_t stream_adj_pass_f32(const StreamAdjArgs& a);
+hipError_t stream_adj_pass_bf16(const StreamAdjArgs& a);
+inline hipError_t stream_adj_pass(const StreamAdjArgs& a) {
+  return a.dtype == 0 ? stream_adj_pass_f32(a) : stream_adj_pass_bf16(a);
+}
+
+struct GradFinishArgs {
+  const void* x;
+  const void* lam;
+  const void* dy;
+  const float* gsum;
+  const float* hsum;
+  void* dx;
+  void* dlam;
+  void* du;
+  int64_t n;
+  int dtype;
+  void* stream;
+};
+hipError_t grad_finish_f32(const GradFinishArgs& a);
+hipError_t grad_finish_bf16(const GradFinishArgs& a);
+inline hipError_t grad_finish(const GradFinishArgs& a) {
+  return a.dtype == 0 ? grad_finish_f32(a) : grad_finish_bf16(a);
+}
+
+}  // namespace gspn

@@ -1,0 +1,147 @@
+"""C ABI contract checks that need no GPU.
+
+The library must load, export every function include/gspn.h declares, size
+workspaces on the host, and reject bad arguments before touching the device
+(every call below returns from host-side validation; none launches a kernel).
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gspn.h")
+
+L = pytest.importorskip("paper_2501_12381_amd.lib")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(L.LIB_PATH):
+        pytest.fail("libgspn.so is not built (run __graft_entry__.build())")
+    return L.load()
+
+
+def header_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(gspn_[a-z_0-9]+)\s*\(", src)))
+
+
+def test_header_declares_expected_api():
+    assert header_functions() == sorted(L.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in header_functions():
+        assert hasattr(lib, name), name
+        assert ctypes.cast(getattr(lib, name), ctypes.c_void_p).value
+
+
+def test_header_constants_match_binding():
+    src = open(HEADER).read()
+    consts = dict(re.findall(r"\b(GSPN_[A-Z0-9_]+)\s*=\s*(\d+)u?", src))
+    for name in ("GSPN_F32", "GSPN_BF16", "GSPN_DIR_T2B", "GSPN_DIR_B2T", "GSPN_DIR_L2R",
+                 "GSPN_DIR_R2L", "GSPN_ALGO_AUTO", "GSPN_ALGO_RESIDENT", "GSPN_ALGO_STREAM"):
+        assert int(consts[name]) == getattr(L, name), name
+    for code, name in L.STATUS.items():
+        assert int(consts[name]) == code, name
+    assert int(re.search(r"#define GSPN_MAX_LINE (\d+)", src).group(1)) == L.GSPN_MAX_LINE
+
+
+def test_strerror_and_version(lib):
+    for code in list(L.STATUS) + [42, -1]:
+        s = L.gspn_strerror(code)
+        assert isinstance(s, str) and s
+    assert L.gspn_strerror(0) == "success"
+    assert L.gspn_version() >= 100
+
+
+def test_workspace_sizes():
+    f32, bf = L.GSPN_F32, L.GSPN_BF16
+    S = L.GSPN_ALGO_STREAM
+    npc = 2 * 3 * 5 * 7
+    # streaming forward: one fp32 accumulator when several directions are merged
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 7, 0x1, f32, S) == 0
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 7, 0xF, bf, S) >= npc * 4
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 7, 0xF, bf, S) % 256 == 0
+    # streaming backward: previous-line state, sum of h, sum of g (fp32 each)
+    assert L.gspn_scan_bwd_workspace_bytes(2, 3, 5, 7, 0xF, f32, S) >= 3 * npc * 4
+    # invalid problems report 0
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 7, 0, f32, S) == 0
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 7, 1, 7, S) == 0
+    assert L.gspn_scan_fwd_workspace_bytes(0, 3, 5, 7, 0xF, f32, S) == 0
+
+
+FAKE = 1 << 40  # never dereferenced: every call below fails validation first
+
+
+def _no_gpu():
+    """Fake-pointer calls run only where no GPU exists, so a validation slip can
+    never turn into a launch on real hardware."""
+    try:
+        import torch
+        if torch.cuda.is_available():
+            pytest.skip("host-validation checks with fake pointers run only without a GPU")
+    except ImportError:
+        pass
+
+
+def fwd(x=FAKE, w=FAKE + (1 << 30), lam=FAKE + (2 << 30), u=FAKE + (3 << 30), y=FAKE + (4 << 30),
+        B=1, C=2, H=8, W=8, mask=0xF, dtype=L.GSPN_F32, algo=L.GSPN_ALGO_STREAM, ws=FAKE + (5 << 30),
+        ws_bytes=1 << 20):
+    return L.gspn_scan_fwd(x, w, lam, u, y, B, C, H, W, mask, dtype, algo, ws, ws_bytes, None)
+
+
+def test_fwd_rejects_bad_arguments(lib):
+    _no_gpu()
+    assert fwd(mask=0) == 3
+    assert fwd(mask=16) == 3
+    assert fwd(dtype=2) == 4
+    assert fwd(algo=9) == 7
+    assert fwd(B=-1) == 2
+    assert fwd(B=1 << 40, C=1 << 40) == 2  # element count overflows int64
+    assert fwd(x=None) == 1
+    assert fwd(y=None) == 1
+    assert fwd(x=FAKE + 2) == 5  # fp32 needs 4-byte alignment
+    assert fwd(dtype=L.GSPN_BF16, x=FAKE + 1) == 5
+    assert fwd(y=FAKE + 8) == 6  # y overlaps x
+    assert fwd(y=FAKE + (1 << 30) + 64) == 6  # y inside w
+    assert fwd(H=L.GSPN_MAX_LINE + 1) == 7
+    assert fwd(ws=None) == 8
+    assert fwd(ws_bytes=16) == 8
+    assert fwd(ws=FAKE + (5 << 30) + 64) == 5  # workspace must be 256-byte aligned
+    assert fwd(ws=FAKE + 256) == 6  # workspace overlaps x (x spans 512 bytes)
+    assert fwd(algo=L.GSPN_ALGO_RESIDENT, H=4096, W=4096) == 7
+
+
+def test_empty_problem_is_a_noop(lib):
+    _no_gpu()
+    # nothing to compute: OK without looking at the pointers
+    assert fwd(B=0, x=None, y=None) == 0
+    assert fwd(H=0, x=None, y=None, ws=None) == 0
+
+
+def test_bwd_rejects_bad_arguments(lib):
+    _no_gpu()
+    base = [FAKE + (k << 30) for k in range(10)]
+
+    def bwd(**kw):
+        p = dict(zip(["dy", "x", "w", "lam", "u", "dx", "dw", "dlam", "du", "ws"], base))
+        p.update({k: v for k, v in kw.items() if k in p})
+        dims = dict(B=1, C=2, H=8, W=8, mask=0xF, dtype=L.GSPN_F32, algo=L.GSPN_ALGO_STREAM,
+                    ws_bytes=1 << 24)
+        dims.update({k: v for k, v in kw.items() if k in dims})
+        return L.gspn_scan_bwd(p["dy"], p["x"], p["w"], p["lam"], p["u"], p["dx"], p["dw"],
+                               p["dlam"], p["du"], dims["B"], dims["C"], dims["H"], dims["W"],
+                               dims["mask"], dims["dtype"], dims["algo"], p["ws"],
+                               dims["ws_bytes"], None)
+
+    assert bwd(mask=0) == 3
+    assert bwd(dtype=5) == 4
+    assert bwd(dw=None) == 1
+    assert bwd(du=base[5]) == 6  # du aliases dx
+    assert bwd(dx=base[0] + 128) == 6  # dx inside dy
+    assert bwd(ws_bytes=100) == 8
+    assert bwd(W=-3) == 2

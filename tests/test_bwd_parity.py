@@ -1,0 +1,117 @@
+"""Backward parity: HIP adjoint scan (through the C ABI) vs the float64 oracle,
+and vs central finite differences of the oracle's loss."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2501_12381_amd import lib as L
+from paper_2501_12381_amd import ops, synth
+from paper_2501_12381_amd.synth import WORKLOADS
+from tests.parity_util import assert_close, np64, oracle_bwd
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+ALGOS = [L.GSPN_ALGO_AUTO, L.GSPN_ALGO_STREAM, L.GSPN_ALGO_RESIDENT]
+ALGO_NAMES = {0: "auto", 1: "resident", 2: "stream"}
+
+
+def run_bwd(inp, mask, algo):
+    try:
+        return ops.gspn_scan_bwd(inp["dy"], inp["x"], inp["w"], inp["lam"], inp["u"], mask, algo=algo)
+    except L.GSPNError as e:
+        if e.status == 7 and algo == L.GSPN_ALGO_RESIDENT:
+            pytest.skip("resident kernel does not take this shape")
+        raise
+
+
+def check_grads(got, ref, dtype, what):
+    dx, dw, dlam, du = got
+    rdx, rdw, rdlam, rdu = ref
+    assert_close(dx, rdx, dtype, f"{what} dx")
+    assert_close(dlam, rdlam, dtype, f"{what} dlam")
+    assert_close(du, rdu, dtype, f"{what} du")
+    for n in range(rdw.shape[0]):
+        for k in range(3):
+            assert_close(dw[n, k], rdw[n, k], dtype, f"{what} dw[{n}][{k}]")
+
+
+@pytest.mark.parametrize("algo", ALGOS, ids=lambda a: ALGO_NAMES[a])
+def test_cls28_fwd_bwd_full(algo):
+    """4-direction forward+backward, bf16, 32x192x28x28."""
+    wl = WORKLOADS["cls28_bf16_fb"]
+    print(f"[bwd] cls28 full algo={ALGO_NAMES[algo]}", flush=True)
+    inp = synth.make_inputs(wl, DEV)
+    got = run_bwd(inp, wl.mask, algo)
+    torch.cuda.synchronize()
+    check_grads(got, oracle_bwd(inp, wl.mask), torch.bfloat16, "cls28")
+
+
+SHAPES = [(1, 1), (1, 6), (6, 1), (2, 3), (5, 7), (7, 5), (16, 16), (28, 28), (9, 65), (65, 9),
+          (3, 130), (130, 3), (4, 300), (300, 4), (2, 1030), (1030, 2), (56, 56)]
+
+
+@pytest.mark.parametrize("algo", ALGOS, ids=lambda a: ALGO_NAMES[a])
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16], ids=["f32", "bf16"])
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: f"{s[0]}x{s[1]}")
+def test_bwd_shapes(shape, dtype, algo):
+    H, W = shape
+    print(f"[bwd] {H}x{W} {dtype} algo={ALGO_NAMES[algo]}", flush=True)
+    t = synth.random_general((2, 3, H, W), 4, device=DEV, seed=H * 31 + W)
+    inp = {k: v.to(dtype) for k, v in t.items()}
+    got = run_bwd(inp, 0xF, algo)
+    torch.cuda.synchronize()
+    check_grads(got, oracle_bwd(inp, 0xF), dtype, f"{H}x{W}")
+
+
+@pytest.mark.parametrize("algo", ALGOS, ids=lambda a: ALGO_NAMES[a])
+@pytest.mark.parametrize("mask", [1, 2, 4, 8, 3, 12, 5, 10, 7, 14, 15])
+def test_bwd_masks(mask, algo):
+    t = synth.random_general((1, 4, 11, 19), ops.n_dirs(mask), device=DEV, seed=100 + mask)
+    got = run_bwd(t, mask, algo)
+    torch.cuda.synchronize()
+    check_grads(got, oracle_bwd(t, mask), torch.float32, f"mask {mask}")
+
+
+@pytest.mark.parametrize("algo", ALGOS, ids=lambda a: ALGO_NAMES[a])
+def test_bwd_matches_oracle_finite_differences(algo):
+    """fp32 GPU gradients vs central differences of the oracle's float64 loss <dy, y>."""
+    H, W, mask = 4, 5, 0xF
+    t = synth.random_general((1, 2, H, W), 4, device=DEV, seed=7)
+    dx, dw, dlam, du = (np64(v) for v in run_bwd(t, mask, algo))
+    a = {k: np64(v) for k, v in t.items()}
+    loss = lambda x, w, lam, u: float((a["dy"] * O.scan_fwd(x, w, lam, u, mask)).sum())
+    eps = 1e-6
+    rng = np.random.default_rng(3)
+    args = [a["x"], a["w"], a["lam"], a["u"]]
+    for which, grad in enumerate((dx, dw, dlam, du)):
+        for _ in range(4):
+            v = rng.standard_normal(args[which].shape)
+            p, m = list(args), list(args)
+            p[which] = args[which] + eps * v
+            m[which] = args[which] - eps * v
+            fd = (loss(*p) - loss(*m)) / (2 * eps)
+            an = float((grad * v).sum())
+            assert abs(fd - an) <= 2e-5 * max(1.0, abs(fd)), (which, fd, an)
+
+
+@pytest.mark.parametrize("algo", ALGOS, ids=lambda a: ALGO_NAMES[a])
+def test_bwd_deterministic(algo):
+    wl = WORKLOADS["cls28_bf16_fb"].with_shape(B=2)
+    inp = synth.make_inputs(wl, DEV)
+    a = run_bwd(inp, wl.mask, algo)
+    b = run_bwd(inp, wl.mask, algo)
+    torch.cuda.synchronize()
+    for u, v in zip(a, b):
+        assert torch.equal(u.view(torch.int16), v.view(torch.int16))
+
+
+def test_autograd_function_matches_oracle():
+    wl = WORKLOADS["cls28_bf16_fb"].with_shape(B=1, C=8)
+    inp = synth.make_inputs(wl, DEV)
+    leaves = {k: inp[k].clone().requires_grad_(True) for k in ("x", "w", "lam", "u")}
+    y = ops.gspn_scan(leaves["x"], leaves["w"], leaves["lam"], leaves["u"], wl.mask)
+    (y.float() * inp["dy"].float()).sum().backward()
+    ref = oracle_bwd(inp, wl.mask)
+    got = (leaves["x"].grad, leaves["w"].grad, leaves["lam"].grad, leaves["u"].grad)
+    check_grads(got, ref, torch.bfloat16, "autograd")
