@@ -91,7 +91,8 @@ enum {
 enum {
   GSPN_ALGO_AUTO = 0,
   GSPN_ALGO_RESIDENT = 1, /* whole plane kept on chip, all directions in one kernel */
-  GSPN_ALGO_STREAM = 2    /* one pass per direction through an fp32 workspace */
+  GSPN_ALGO_STREAM = 2,   /* one pass per direction through an fp32 workspace */
+  GSPN_ALGO_RESIDENT_GENERIC = 3 /* resident family without size-specialised kernels */
 };
 
 /* Bytes of workspace gspn_scan_fwd needs for this problem (0 if none). */

@@ -46,7 +46,7 @@ int check_shape(int64_t B, int64_t C, int64_t H, int64_t W, uint32_t mask, int d
                 Problem* p) {
   if (dtype != GSPN_F32 && dtype != GSPN_BF16) return GSPN_ERR_DTYPE;
   if (mask == 0 || mask > 15u) return GSPN_ERR_MASK;
-  if (algo < GSPN_ALGO_AUTO || algo > GSPN_ALGO_STREAM) return GSPN_ERR_UNSUPPORTED;
+  if (algo < GSPN_ALGO_AUTO || algo > GSPN_ALGO_RESIDENT_GENERIC) return GSPN_ERR_UNSUPPORTED;
   if (B < 0 || C < 0 || H < 0 || W < 0) return GSPN_ERR_SHAPE;
   p->B = B; p->C = C; p->H = H; p->W = W;
   p->n = popcount4(mask);
@@ -105,11 +105,14 @@ bool resident_fits(const Problem& p, int dtype, bool backward);  // defined belo
 
 int choose_algo(const Problem& p, int dtype, int algo, bool backward) {
   if (algo == GSPN_ALGO_STREAM) return GSPN_ALGO_STREAM;
-  if (algo == GSPN_ALGO_RESIDENT) return resident_fits(p, dtype, backward) ? GSPN_ALGO_RESIDENT : -1;
+  if (algo == GSPN_ALGO_RESIDENT || algo == GSPN_ALGO_RESIDENT_GENERIC)
+    return resident_fits(p, dtype, backward) ? algo : -1;
   return resident_fits(p, dtype, backward) ? GSPN_ALGO_RESIDENT : GSPN_ALGO_STREAM;
 }
 
-bool resident_fits(const Problem&, int, bool) { return false; }
+bool resident_fits(const Problem& p, int dtype, bool backward) {
+  return gspn::resident_fits((int)p.H, (int)p.W, dtype, backward);
+}
 
 size_t fwd_ws_bytes(const Problem& p, int algo) {
   if (algo == GSPN_ALGO_STREAM && p.n > 1) return round_up((size_t)p.npc * 4, kWsAlign);
@@ -159,6 +162,14 @@ int gspn_scan_fwd(const void* x, const void* w, const void* lam, const void* u, 
   st = check_ws(workspace, workspace_bytes, need, {{x, tb}, {w, wb}, {lam, tb}, {u, tb}, {y, tb}});
   if (st != GSPN_OK) return st;
 
+  if (a == GSPN_ALGO_RESIDENT || a == GSPN_ALGO_RESIDENT_GENERIC) {
+    ResidentFwdArgs r{};
+    r.x = x; r.lam = lam; r.w = w; r.u = u; r.y = y;
+    r.mask = mask; r.planes = p.planes; r.H = (int)H; r.W = (int)W; r.dtype = dtype;
+    r.use_fixed = a == GSPN_ALGO_RESIDENT;
+    r.stream = stream;
+    return hip_status(resident_fwd(r));
+  }
   const std::vector<int> ds = dirs_of(mask);
   const int n = (int)ds.size();
   for (int i = 0; i < n; ++i) {

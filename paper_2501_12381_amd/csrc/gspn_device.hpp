@@ -102,4 +102,12 @@ __device__ __forceinline__ float from_next_lane(float v) {
                                                                0x130 /* wave_shl:1 */, 0xf, 0xf, false));
 }
 
+// Workgroup barrier that orders LDS accesses only: waits for this wave's LDS
+// operations, then for every wave.  Global loads stay in flight across it
+// (a full __syncthreads would drain them), which keeps register prefetches
+// useful across the barriers of a scan.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 }  // namespace gspn

@@ -71,4 +71,24 @@ inline hipError_t grad_finish(const GradFinishArgs& a) {
   return a.dtype == 0 ? grad_finish_f32(a) : grad_finish_bf16(a);
 }
 
+// ---- resident family: whole planes on chip, all directions in one launch ----
+struct ResidentFwdArgs {
+  const void* x;
+  const void* lam;
+  const void* w;   // all n directions, packed [n][3][B][C][H][W]
+  const void* u;
+  void* y;
+  uint32_t mask;
+  int64_t planes;
+  int H, W, dtype;
+  int use_fixed;   // allow the size-specialised kernel when one exists for H x W
+  void* stream;
+};
+hipError_t resident_fwd_f32(const ResidentFwdArgs& a);
+hipError_t resident_fwd_bf16(const ResidentFwdArgs& a);
+inline hipError_t resident_fwd(const ResidentFwdArgs& a) {
+  return a.dtype == 0 ? resident_fwd_f32(a) : resident_fwd_bf16(a);
+}
+bool resident_fits(int H, int W, int dtype, bool backward);
+
 }  // namespace gspn

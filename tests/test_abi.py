@@ -43,7 +43,8 @@ def test_header_constants_match_binding():
     src = open(HEADER).read()
     consts = dict(re.findall(r"\b(GSPN_[A-Z0-9_]+)\s*=\s*(\d+)u?", src))
     for name in ("GSPN_F32", "GSPN_BF16", "GSPN_DIR_T2B", "GSPN_DIR_B2T", "GSPN_DIR_L2R",
-                 "GSPN_DIR_R2L", "GSPN_ALGO_AUTO", "GSPN_ALGO_RESIDENT", "GSPN_ALGO_STREAM"):
+                 "GSPN_DIR_R2L", "GSPN_ALGO_AUTO", "GSPN_ALGO_RESIDENT", "GSPN_ALGO_STREAM",
+                 "GSPN_ALGO_RESIDENT_GENERIC"):
         assert int(consts[name]) == getattr(L, name), name
     for code, name in L.STATUS.items():
         assert int(consts[name]) == code, name

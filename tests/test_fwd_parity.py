@@ -11,15 +11,15 @@ from tests.parity_util import TOL, assert_close, np64, oracle_fwd
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
-ALGOS = [L.GSPN_ALGO_AUTO, L.GSPN_ALGO_STREAM, L.GSPN_ALGO_RESIDENT]
-ALGO_NAMES = {0: "auto", 1: "resident", 2: "stream"}
+ALGOS = [L.GSPN_ALGO_AUTO, L.GSPN_ALGO_STREAM, L.GSPN_ALGO_RESIDENT, L.GSPN_ALGO_RESIDENT_GENERIC]
+ALGO_NAMES = {0: "auto", 1: "resident", 2: "stream", 3: "resident_generic"}
 
 
 def run_fwd(inp, mask, algo):
     try:
         return ops.gspn_scan_fwd(inp["x"], inp["w"], inp["lam"], inp["u"], mask, algo=algo)
     except L.GSPNError as e:
-        if e.status == 7 and algo == L.GSPN_ALGO_RESIDENT:
+        if e.status == 7 and algo in (L.GSPN_ALGO_RESIDENT, L.GSPN_ALGO_RESIDENT_GENERIC):
             pytest.skip("resident kernel does not take this shape")
         raise
 
