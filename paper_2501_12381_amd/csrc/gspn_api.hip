@@ -201,13 +201,30 @@ int gspn_scan_bwd(const void* dy, const void* x, const void* w, const void* lam,
   st = check_ptrs({{dy, tb}, {x, tb}, {w, wb}, {lam, tb}, {u, tb}},
                   {{dx, tb}, {dw, wb}, {dlam, tb}, {du, tb}}, es);
   if (st != GSPN_OK) return st;
-  const int a = choose_algo(p, dtype, algo, true);
+  int a = choose_algo(p, dtype, algo, true);
   if (a < 0) return GSPN_ERR_UNSUPPORTED;
+  if (a == GSPN_ALGO_RESIDENT || a == GSPN_ALGO_RESIDENT_GENERIC) {
+    // the resident backward reads and writes 16-byte vectors
+    for (const void* q : {dy, x, w, lam, u, (const void*)dx, (const void*)dw, (const void*)dlam, (const void*)du})
+      if ((uintptr_t)q % 16) {
+        if (algo != GSPN_ALGO_AUTO) return GSPN_ERR_ALIGN;
+        a = GSPN_ALGO_STREAM;  // needs the streaming workspace (size it with GSPN_ALGO_STREAM)
+        break;
+      }
+  }
   const size_t need = bwd_ws_bytes(p, a);
   st = check_ws(workspace, workspace_bytes, need,
                 {{dy, tb}, {x, tb}, {w, wb}, {lam, tb}, {u, tb}, {dx, tb}, {dw, wb}, {dlam, tb}, {du, tb}});
   if (st != GSPN_OK) return st;
 
+  if (a == GSPN_ALGO_RESIDENT || a == GSPN_ALGO_RESIDENT_GENERIC) {
+    ResidentBwdArgs r{};
+    r.dy = dy; r.x = x; r.lam = lam; r.w = w; r.u = u;
+    r.dx = dx; r.dw = dw; r.dlam = dlam; r.du = du;
+    r.mask = mask; r.planes = p.planes; r.H = (int)H; r.W = (int)W; r.dtype = dtype;
+    r.stream = stream;
+    return hip_status(resident_bwd(r));
+  }
   const size_t fb = round_up((size_t)p.npc * 4, kWsAlign);
   float* hprev = (float*)workspace;
   float* hsum = (float*)((char*)workspace + fb);

@@ -89,6 +89,26 @@ hipError_t resident_fwd_bf16(const ResidentFwdArgs& a);
 inline hipError_t resident_fwd(const ResidentFwdArgs& a) {
   return a.dtype == 0 ? resident_fwd_f32(a) : resident_fwd_bf16(a);
 }
+struct ResidentBwdArgs {
+  const void* dy;
+  const void* x;
+  const void* lam;
+  const void* w;
+  const void* u;
+  void* dx;
+  void* dw;
+  void* dlam;
+  void* du;
+  uint32_t mask;
+  int64_t planes;
+  int H, W, dtype;
+  void* stream;
+};
+hipError_t resident_bwd_f32(const ResidentBwdArgs& a);
+hipError_t resident_bwd_bf16(const ResidentBwdArgs& a);
+inline hipError_t resident_bwd(const ResidentBwdArgs& a) {
+  return a.dtype == 0 ? resident_bwd_f32(a) : resident_bwd_bf16(a);
+}
 bool resident_fits(int H, int W, int dtype, bool backward);
 
 }  // namespace gspn
