@@ -125,6 +125,15 @@ int gspn_scan_bwd(const void* dy, const void* x, const void* w, const void* lam,
                   int64_t B, int64_t C, int64_t H, int64_t W, uint32_t mask, int dtype,
                   int algo, void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * Plain device-to-device copy of `bytes` bytes (src and dst 16-byte aligned,
+ * not overlapping).  Not part of the scan: it is the reference kernel of known
+ * traffic (reads `bytes`, writes `bytes`) against which hardware byte counters
+ * (rocprofv3 FETCH_SIZE / WRITE_SIZE) of the scan kernels are scaled.
+ * Asynchronous on `stream`.
+ */
+int gspn_copy_calibration(const void* src, void* dst, size_t bytes, void* stream);
+
 /* Static, NUL-terminated description of a status code. */
 const char* gspn_strerror(int status);
 

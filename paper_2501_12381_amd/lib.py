@@ -22,7 +22,7 @@ STATUS = {0: "GSPN_OK", 1: "GSPN_ERR_NULL", 2: "GSPN_ERR_SHAPE", 3: "GSPN_ERR_MA
 
 # every symbol include/gspn.h declares
 EXPORTS = ("gspn_scan_fwd_workspace_bytes", "gspn_scan_fwd", "gspn_scan_bwd_workspace_bytes",
-           "gspn_scan_bwd", "gspn_strerror", "gspn_version")
+           "gspn_scan_bwd", "gspn_copy_calibration", "gspn_strerror", "gspn_version")
 
 _lib = None
 
@@ -53,6 +53,8 @@ def load() -> ctypes.CDLL:
     lib.gspn_scan_bwd.argtypes = [_p, _p, _p, _p, _p, _p, _p, _p, _p, _i64, _i64, _i64, _i64, _u32,
                                   _i, _i, _p, _sz, _p]
     lib.gspn_scan_bwd.restype = _i
+    lib.gspn_copy_calibration.argtypes = [_p, _p, _sz, _p]
+    lib.gspn_copy_calibration.restype = _i
     lib.gspn_strerror.argtypes = [_i]
     lib.gspn_strerror.restype = ctypes.c_char_p
     lib.gspn_version.argtypes = []
@@ -79,6 +81,10 @@ def gspn_scan_bwd(dy, x, w, lam, u, dx, dw, dlam, du, B, C, H, W, mask, dtype, a
                   workspace_bytes, stream) -> int:
     return int(load().gspn_scan_bwd(dy, x, w, lam, u, dx, dw, dlam, du, B, C, H, W, mask, dtype,
                                     algo, workspace, workspace_bytes, stream))
+
+
+def gspn_copy_calibration(src, dst, nbytes, stream) -> int:
+    return int(load().gspn_copy_calibration(src, dst, nbytes, stream))
 
 
 def gspn_strerror(status: int) -> str:

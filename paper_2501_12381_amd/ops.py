@@ -112,3 +112,16 @@ class GSPNScan(torch.autograd.Function):
 def gspn_scan(x, w, lam, u, mask: int = 0xF, algo: int = L.GSPN_ALGO_AUTO) -> torch.Tensor:
     """Differentiable 4-direction (or masked) GSPN line scan."""
     return GSPNScan.apply(x, w, lam, u, mask, algo)
+
+
+def gspn_copy_calibration(src: torch.Tensor, dst: torch.Tensor) -> None:
+    """Copy src into dst with the library's reference copy kernel (known traffic)."""
+    if src.device.type != "cuda" or dst.device != src.device:
+        raise RuntimeError("gspn_copy_calibration runs on the GPU only")
+    n = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() < n:
+        raise ValueError("dst is smaller than src")
+    with torch.cuda.device(src.device):
+        st = L.gspn_copy_calibration(src.data_ptr(), dst.data_ptr(), n, _stream(src.device))
+    if st != 0:
+        raise L.GSPNError(st, "gspn_copy_calibration")

@@ -140,3 +140,11 @@ def test_errors_surface_as_exceptions():
         ops.gspn_scan_fwd(big, torch.zeros(1, 3, 1, 1, 1, L.GSPN_MAX_LINE + 1, device=DEV), big,
                           big, 1)
     assert ei.value.status == 7
+
+
+def test_copy_calibration_kernel():
+    src = torch.randint(0, 255, (3 * 1024 * 1024 + 37,), dtype=torch.uint8, device=DEV)
+    dst = torch.zeros_like(src)
+    ops.gspn_copy_calibration(src[:-5], dst[:-5])  # 16-byte aligned starts, ragged tail
+    torch.cuda.synchronize()
+    assert torch.equal(dst[:-5], src[:-5]) and not dst[-5:].any()
