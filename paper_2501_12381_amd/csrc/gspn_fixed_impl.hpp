@@ -8,10 +8,10 @@
 //   * every global and LDS address of a line is a base register plus an
 //     immediate offset, so a line step carries no address arithmetic;
 //   * phases of up to 64 lines are fully unrolled (the middle barrier and the
-//     padding masks resolve at compile time); 128-line phases run chunks of 16
+//     padding masks resolve at compile time); 128-line phases run chunks of 64
 //     lines whose boundary falls on the middle line;
 //   * inputs are prefetched through a register ring of R tiles (a tile is one
-//     row for vertical scans, a VL-column row segment for horizontal ones);
+//     row for vertical scans, a row segment of THZ columns for horizontal ones);
 //   * accumulator values are read G lines ahead of their update, never across
 //     the middle barrier, so LDS latency stays off the critical path.
 #pragma once
@@ -31,12 +31,17 @@ struct FixedCfg {
   static constexpr int ROWS = S + 1;                             // + padding row
   static constexpr int MID = S / 2;
   static constexpr bool FULL = S <= 64;                          // fully unrolled phases
-  static constexpr int CHUNK = FULL ? S : 16;                    // lines per loop iteration
+  static constexpr int CHUNK = FULL ? S : 64;                    // lines per loop iteration
   // horizontal vector: largest of 16/8/4 bytes whose element count divides S
   static constexpr int VLH = (S % (16 / (int)sizeof(T)) == 0) ? 16 / (int)sizeof(T)
                            : (S % (8 / (int)sizeof(T)) == 0 ? 8 / (int)sizeof(T) : 4 / (int)sizeof(T));
+  // horizontal tile: lines per row segment.  Long planes read 128-byte row
+  // segments (eight 16-byte vectors back to back, one tile in flight) so every
+  // cache line fetched for a row is consumed by the same load; shorter segments
+  // let the line be evicted before its neighbours are read and fetch it again.
+  static constexpr int THZ = FULL ? VLH : 128 / (int)sizeof(T);
   static constexpr int RV = FULL ? (S % 8 == 0 ? 8 : 7) : 8;     // vertical ring (lines)
-  static constexpr int RH = FULL ? 6 : 2;                         // horizontal ring (tiles)
+  static constexpr int RH = FULL ? 6 : 1;                         // horizontal ring (tiles)
   static constexpr int G = 4;                                     // accumulator lookahead
   static constexpr bool ALL_VALID = (S == SEG * NP);
   static constexpr int LDS_BYTES = PPW * ROWS * P * 4;
@@ -51,7 +56,7 @@ __device__ __forceinline__ void fixed_phase(const T* const (&pbase)[5], float* _
                                             int sl) {
   using C = FixedCfg<T, S>;
   constexpr int NP = C::NP;
-  constexpr int TL = HZ ? C::VLH : 1;   // lines per tile
+  constexpr int TL = HZ ? C::THZ : 1;   // lines per tile
   constexpr int R = HZ ? C::RH : C::RV; // tiles in flight
   constexpr int NT = S / TL;            // tiles per phase
   constexpr int CT = C::CHUNK / TL;     // tiles per chunk
@@ -120,21 +125,27 @@ __device__ __forceinline__ void fixed_phase(const T* const (&pbase)[5], float* _
     for (int k = 0; k < CT; ++k) {
       const int ti = c * CT + k;
       const int slot = k % R;
-      float v[5][TL][NP];
+      // vertical tiles are one line: unpack and refill the slot at once; horizontal
+      // tiles are unpacked line by line and the slot is refilled after its last line
+      float v1[5][NP];
+      if constexpr (!HZ) {
 #pragma unroll
-      for (int m = 0; m < 5; ++m)
+        for (int m = 0; m < 5; ++m)
 #pragma unroll
-        for (int e = 0; e < TL; ++e)
-#pragma unroll
-          for (int q = 0; q < NP; ++q)
-            v[m][e][q] = HZ ? ring[slot][m][q].get(e) : ring[slot][m][0].get(q);
-      load_tile(ring[slot], ti + R);  // clamped to the last tile past the end
+          for (int q = 0; q < NP; ++q) v1[m][q] = ring[slot][m][0].get(q);
+        load_tile(ring[slot], ti + R);  // clamped to the last tile past the end
+      }
 #pragma unroll
       for (int ee = 0; ee < TL; ++ee) {
         const int e = REV ? TL - 1 - ee : ee;  // memory order inside the tile
         const int kk = k * TL + ee;            // step inside the chunk
         const int s = s_base + kk;             // step inside the phase
-        line_step<NP>(v[0][e], v[1][e], v[2][e], v[3][e], v[4][e], valid, hp);
+        float v[5][NP];
+#pragma unroll
+        for (int m = 0; m < 5; ++m)
+#pragma unroll
+          for (int q = 0; q < NP; ++q) v[m][q] = HZ ? ring[slot][m][q].get(e) : v1[m][q];
+        line_step<NP>(v[0], v[1], v[2], v[3], v[4], valid, hp);
         const int gi = kk % C::G;
         const int line = line_of(s);
         if (C::FULL && s == C::MID) {
@@ -160,6 +171,7 @@ __device__ __forceinline__ void fixed_phase(const T* const (&pbase)[5], float* _
           if (kk + C::G < C::CHUNK && sn < S && !cross) acc_read(av[gi], sn);
         }
       }
+      if constexpr (HZ) load_tile(ring[slot], ti + R);
     }
   };
 
