@@ -12,7 +12,7 @@ dominant kernel (algorithmic HBM bytes / its average duration, timed with
 events on the stream it runs on) and the float64 CPU oracle timed on a bounded
 sample of the same workload.
 
-    python bench.py [--steps K] [--warmup W] [--workload NAME] [--algo auto|resident|stream]
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--algo auto|resident|stream|two_pass]
 """
 from __future__ import annotations
 
@@ -29,7 +29,7 @@ sys.path.insert(0, ROOT)
 METRIC = "propagated pixel-channel-directions/sec and % of HBM roofline, fwd and fwd+bwd"
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E peak
 DEFAULT_WORKLOAD = "cls28_bf16_fb"  # the workload whose step covers forward and backward
-ALGOS = {"auto": 0, "resident": 1, "stream": 2, "resident_generic": 3}
+ALGOS = {"auto": 0, "resident": 1, "stream": 2, "resident_generic": 3, "two_pass": 4}
 KERNEL_SRC = os.path.join(ROOT, "paper_2501_12381_amd", "csrc")
 
 

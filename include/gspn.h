@@ -92,7 +92,13 @@ enum {
   GSPN_ALGO_AUTO = 0,
   GSPN_ALGO_RESIDENT = 1, /* whole plane kept on chip, all directions in one kernel */
   GSPN_ALGO_STREAM = 2,   /* one pass per direction through an fp32 workspace */
-  GSPN_ALGO_RESIDENT_GENERIC = 3 /* resident family without size-specialised kernels */
+  GSPN_ALGO_RESIDENT_GENERIC = 3, /* resident family without size-specialised kernels */
+  GSPN_ALGO_TWO_PASS = 4 /* forward only, for planes too large to keep on chip: the
+                            vertical pair of directions in one pass, the horizontal
+                            pair in blocks of 128-byte columns, partial sums in an
+                            fp32 workspace.  Needs W * element size a multiple of
+                            16 bytes and at least 128 bytes, W <= 4096 (bf16) or
+                            2048 (f32), and 16-byte aligned x, w, lam, u, y. */
 };
 
 /* Bytes of workspace gspn_scan_fwd needs for this problem (0 if none). */

@@ -1,5 +1,6 @@
 // C ABI of the GSPN line scan: argument checking, workspace sizing and dispatch.
-// Host code only; the kernels live in gspn_stream.hip and gspn_resident.hip.
+// Host code only; the kernels live in the gspn_stream_*, gspn_resident_* and
+// gspn_large_* sources.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -46,7 +47,7 @@ int check_shape(int64_t B, int64_t C, int64_t H, int64_t W, uint32_t mask, int d
                 Problem* p) {
   if (dtype != GSPN_F32 && dtype != GSPN_BF16) return GSPN_ERR_DTYPE;
   if (mask == 0 || mask > 15u) return GSPN_ERR_MASK;
-  if (algo < GSPN_ALGO_AUTO || algo > GSPN_ALGO_RESIDENT_GENERIC) return GSPN_ERR_UNSUPPORTED;
+  if (algo < GSPN_ALGO_AUTO || algo > GSPN_ALGO_TWO_PASS) return GSPN_ERR_UNSUPPORTED;
   if (B < 0 || C < 0 || H < 0 || W < 0) return GSPN_ERR_SHAPE;
   p->B = B; p->C = C; p->H = H; p->W = W;
   p->n = popcount4(mask);
@@ -103,19 +104,33 @@ int check_ws(void* ws, size_t ws_bytes, size_t need,
 
 bool resident_fits(const Problem& p, int dtype, bool backward);  // defined below
 
+bool two_pass_fits(const Problem& p, int dtype, bool backward) {
+  return !backward && gspn::large_fwd_fits((int)p.H, (int)p.W, dtype);
+}
+
 int choose_algo(const Problem& p, int dtype, int algo, bool backward) {
   if (algo == GSPN_ALGO_STREAM) return GSPN_ALGO_STREAM;
   if (algo == GSPN_ALGO_RESIDENT || algo == GSPN_ALGO_RESIDENT_GENERIC)
     return resident_fits(p, dtype, backward) ? algo : -1;
-  return resident_fits(p, dtype, backward) ? GSPN_ALGO_RESIDENT : GSPN_ALGO_STREAM;
+  if (algo == GSPN_ALGO_TWO_PASS) return two_pass_fits(p, dtype, backward) ? algo : -1;
+  if (resident_fits(p, dtype, backward)) return GSPN_ALGO_RESIDENT;
+  return two_pass_fits(p, dtype, backward) ? GSPN_ALGO_TWO_PASS : GSPN_ALGO_STREAM;
 }
 
 bool resident_fits(const Problem& p, int dtype, bool backward) {
   return gspn::resident_fits((int)p.H, (int)p.W, dtype, backward);
 }
 
-size_t fwd_ws_bytes(const Problem& p, int algo) {
+// two-pass layout: fp32 partial sums (n > 1), then the column state of the
+// horizontal pass (2 parities x 2 directions x planes x H floats)
+size_t two_pass_acc_bytes(const Problem& p) { return p.n > 1 ? round_up((size_t)p.npc * 4, kWsAlign) : 0; }
+size_t two_pass_state_bytes(const Problem& p, uint32_t mask) {
+  return (mask & (DIR_L2R | DIR_R2L)) ? round_up((size_t)4 * p.planes * p.H * 4, kWsAlign) : 0;
+}
+
+size_t fwd_ws_bytes(const Problem& p, int algo, uint32_t mask) {
   if (algo == GSPN_ALGO_STREAM && p.n > 1) return round_up((size_t)p.npc * 4, kWsAlign);
+  if (algo == GSPN_ALGO_TWO_PASS) return two_pass_acc_bytes(p) + two_pass_state_bytes(p, mask);
   return 0;
 }
 
@@ -135,7 +150,7 @@ size_t gspn_scan_fwd_workspace_bytes(int64_t B, int64_t C, int64_t H, int64_t W,
   Problem p;
   if (check_shape(B, C, H, W, mask, dtype, algo, &p) != GSPN_OK || p.empty) return 0;
   const int a = choose_algo(p, dtype, algo, false);
-  return a < 0 ? 0 : fwd_ws_bytes(p, a);
+  return a < 0 ? 0 : fwd_ws_bytes(p, a, mask);
 }
 
 size_t gspn_scan_bwd_workspace_bytes(int64_t B, int64_t C, int64_t H, int64_t W, uint32_t mask,
@@ -156,9 +171,18 @@ int gspn_scan_fwd(const void* x, const void* w, const void* lam, const void* u, 
   const size_t tb = (size_t)p.npc * es, wb = tb * 3 * (size_t)p.n;
   st = check_ptrs({{x, tb}, {w, wb}, {lam, tb}, {u, tb}}, {{y, tb}}, es);
   if (st != GSPN_OK) return st;
-  const int a = choose_algo(p, dtype, algo, false);
+  int a = choose_algo(p, dtype, algo, false);
   if (a < 0) return GSPN_ERR_UNSUPPORTED;
-  const size_t need = fwd_ws_bytes(p, a);
+  if (a == GSPN_ALGO_TWO_PASS) {
+    // the two-pass kernels read and write 16-byte vectors
+    for (const void* q : {x, w, lam, u, (const void*)y})
+      if ((uintptr_t)q % 16) {
+        if (algo != GSPN_ALGO_AUTO) return GSPN_ERR_ALIGN;
+        a = GSPN_ALGO_STREAM;  // its workspace is never larger than the two-pass one
+        break;
+      }
+  }
+  const size_t need = fwd_ws_bytes(p, a, mask);
   st = check_ws(workspace, workspace_bytes, need, {{x, tb}, {w, wb}, {lam, tb}, {u, tb}, {y, tb}});
   if (st != GSPN_OK) return st;
 
@@ -169,6 +193,15 @@ int gspn_scan_fwd(const void* x, const void* w, const void* lam, const void* u, 
     r.use_fixed = a == GSPN_ALGO_RESIDENT;
     r.stream = stream;
     return hip_status(resident_fwd(r));
+  }
+  if (a == GSPN_ALGO_TWO_PASS) {
+    LargeFwdArgs l{};
+    l.x = x; l.lam = lam; l.w = w; l.u = u; l.y = y;
+    l.acc = (float*)workspace;
+    l.state = (float*)((char*)workspace + two_pass_acc_bytes(p));
+    l.mask = mask; l.planes = p.planes; l.H = (int)H; l.W = (int)W; l.dtype = dtype;
+    l.stream = stream;
+    return hip_status(large_fwd(l));
   }
   const std::vector<int> ds = dirs_of(mask);
   const int n = (int)ds.size();

@@ -1,0 +1,559 @@
+// Two-pass forward for planes too large to keep on chip (e.g. 2048 x 2048).
+//
+// The four directions cannot share one sweep (their dependency orders
+// conflict), so sum_d h_d goes through an fp32 workspace `acc` twice:
+//
+//   pass V  (one launch): a workgroup per plane; half of its waves run
+//           top-to-bottom, the other half bottom-to-top.  A row is spread over
+//           the waves of its direction, each lane owning 32 bytes of
+//           positions; the three-way neighbours come from the adjacent lanes
+//           (DPP) and, at wave edges, from an LDS exchange with one barrier per
+//           row.  Each direction stores h for the rows it reaches first; after
+//           the middle row it adds its h to what the other direction stored.
+//   pass H  (one launch per block of K columns, K = 128 bytes of a row):
+//           left-to-right and right-to-left.  A workgroup owns a band of rows
+//           plus a halo of K rows on each side, one row per lane, and holds the
+//           block's K columns of each input as 128-byte row segments in
+//           registers, so every cache line of a row is read by one load.
+//           Starting from the exact state of the previous block (a column of
+//           h per direction, passed between launches in a small workspace),
+//           the halo rows shrink the exact region by one row per column and
+//           leave it equal to the band after K columns.  The band's h goes to
+//           LDS and is added to acc (first half of the blocks) or combined
+//           into y = u * (acc + h) (second half) with coalesced accesses.
+//
+// Both passes pair opposite directions with the same middle-line rule as the
+// resident kernels, so every addition happens in a fixed order and results
+// are reproducible run to run.
+#pragma once
+
+#include <type_traits>
+
+#include "gspn_device.hpp"
+#include "gspn_launch.hpp"
+#include "gspn_resident_impl.hpp"
+
+namespace gspn {
+
+template <typename T>
+struct LargeCfg {
+  static constexpr int VE = 16 / (int)sizeof(T);   // elements per 16-byte vector
+  static constexpr int NPV = 2 * VE;               // vertical: positions per lane (32 bytes)
+  static constexpr int RV = 2;                     // vertical prefetch depth of the inputs (rows)
+  static constexpr int RA = 2;                     // ... of acc and u in the second half
+  static constexpr int KH = 128 / (int)sizeof(T);  // horizontal block: columns per launch
+  static constexpr int HV = KH / VE;               // 16-byte vectors per row segment
+  static constexpr int HROWS = 512;                // rows (lanes) per horizontal workgroup
+  static constexpr int MAX_WPD = 4;                // vertical: waves per direction
+  static constexpr int MAX_W = MAX_WPD * 64 * NPV; // widest row of the vertical pass
+};
+
+// Two 16-byte vectors of a lane: positions [0, VE) at p, [VE, 2 VE) at p + hoff
+// (hoff = 0 re-reads the first vector when the row ends after it).
+template <typename T>
+struct Pack2 {
+  static constexpr int VE = LargeCfg<T>::VE;
+  static constexpr int kWords = 2 * Pack<T, VE>::kWords;
+  Pack<T, VE> a, b;
+  __device__ __forceinline__ void load(const T* __restrict__ p, int hoff) {
+    a.load(p);
+    b.load(p + hoff);
+  }
+  __device__ __forceinline__ float get(int q) const { return q < VE ? a.get(q) : b.get(q - VE); }
+  __device__ __forceinline__ void pin_use() const {
+#pragma unroll
+    for (int i = 0; i < Pack<T, VE>::kWords; ++i) {
+      asm volatile("" ::"v"(a.w[i]));
+      asm volatile("" ::"v"(b.w[i]));
+    }
+  }
+};
+
+// ---------------------------------------------------------------------------
+// pass V
+// ---------------------------------------------------------------------------
+struct LargeVParams {
+  const void* x;
+  const void* lam;
+  const void* w;     // packed [n][3][planes][H][W]
+  const void* u;
+  void* y;
+  float* acc;
+  int64_t planes, npc;
+  int H, W;
+  int slot0, slot1;  // weight slot of top-to-bottom / bottom-to-top, -1 when absent
+  int final_out;     // nonzero: write y = u * sum; zero: write the fp32 partial sum
+};
+
+// BOTH: both vertical directions are present; FIN: write y (no pass H follows)
+template <typename T, int WPD, bool BOTH, bool FIN>
+__global__ void __launch_bounds__(128 * WPD, 2) large_v_kernel(LargeVParams p) {
+  using C = LargeCfg<T>;
+  constexpr int NP = C::NPV, R = C::RV, RA = C::RA;
+  static_assert(R % RA == 0, "acc ring slots must repeat with the input ring");
+  constexpr int VE = C::VE;
+  typedef Pack2<T> PK;
+  static_assert(NP == 2 * VE, "a lane holds two 16-byte vectors");
+  __shared__ float edge[2][2 * WPD][2];  // [step parity][wave][first, last position]
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  constexpr bool both = BOTH, fin = FIN;
+  const int dir = both ? (wave >= WPD ? 1 : 0) : (p.slot0 >= 0 ? 0 : 1);
+  const int wi = both ? wave - dir * WPD : wave;
+  const int64_t plane = blockIdx.x;
+  const int H = p.H, W = p.W;
+  const int pos0 = (wi * 64 + lane) * NP;
+  const bool lane_ok = pos0 < W;
+  const bool hi_ok = pos0 + VE < W;              // the lane's second vector is in the row
+  const int hoff = hi_ok ? VE : 0;
+  const int64_t pb = plane * (int64_t)H * W + (lane_ok ? pos0 : 0);
+  const int slot = dir ? p.slot1 : p.slot0;
+  const int odd = both ? (H & 1) : 0;
+  const int nsteps = H + odd;
+  const int sm = both ? H / 2 + odd : nsteps;  // first step of the second half
+  const int delay = dir ? odd : 0;             // bottom-to-top starts a step late for odd H
+
+  for (int i = threadIdx.x; i < 2 * 2 * WPD * 2; i += blockDim.x) (&edge[0][0][0])[i] = 0.f;
+  __syncthreads();
+
+  const T* w0 = (const T*)p.w + (int64_t)slot * 3 * p.npc;
+  const T* base[5] = {(const T*)p.x + pb, (const T*)p.lam + pb, w0 + pb, w0 + p.npc + pb,
+                      w0 + 2 * p.npc + pb};
+  const T* ubase = (const T*)p.u + pb;
+  const float* abase = p.acc + pb;
+
+  auto t_of = [&](int s) { return s - delay; };
+  auto line_of = [&](int t) {
+    t = t < 0 ? 0 : (t >= H ? H - 1 : t);
+    return dir ? H - 1 - t : t;
+  };
+
+  PK ring[R][5];
+  // Keeps the last prefetches "used" after a loop: without a use the compiler
+  // drains every outstanding load at the top of each iteration.
+  auto consume_ring = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int k = 0; k < R; ++k)
+#pragma unroll
+      for (int m = 0; m < 5; ++m) ring[k][m].pin_use();
+  };
+  auto load_main = [&](PK (&sl)[5], int s) __attribute__((always_inline)) {
+    const int64_t off = (int64_t)line_of(t_of(s)) * W;
+#pragma unroll
+    for (int m = 0; m < 5; ++m) sl[m].load(base[m] + off, hoff);
+  };
+  // second-half (or final single-direction) operands: acc and u of the step's row
+  PK uring[RA];
+  float aring[RA][NP];
+  auto load_aux = [&](int k, int s) __attribute__((always_inline)) {
+    const int64_t off = (int64_t)line_of(t_of(s)) * W;
+    if constexpr (fin) uring[k].load(ubase + off, hoff);
+    if constexpr (both) {
+      ldv<VE>(abase + off, aring[k]);
+      ldv<VE>(abase + off + hoff, aring[k] + VE);
+    }
+  };
+
+  float hp[NP];
+#pragma unroll
+  for (int q = 0; q < NP; ++q) hp[q] = 0.f;
+
+
+  // one step of the scan; SECOND: combine with the other direction's stored h
+  auto step = [&](auto second_tag, int k, int s) __attribute__((always_inline)) {
+    constexpr bool SECOND = decltype(second_tag)::value;
+    const PK(&v)[5] = ring[k];  // unpacked at use; the slot is refilled after the step
+    const int t = t_of(s);
+    const bool act = t >= 0 && t < H;
+    const int par = s & 1;
+    // neighbours of the lane's first and last position on the previous row
+    float el = from_prev_lane(hp[NP - 1]);
+    float er = from_next_lane(hp[0]);
+    if constexpr (WPD > 1) {
+      const float nl = edge[par ^ 1][wi > 0 ? wave - 1 : wave][1];
+      const float nr = edge[par ^ 1][wi < WPD - 1 ? wave + 1 : wave][0];
+      if (lane == 0) el = wi > 0 ? nl : 0.f;
+      if (lane == 63) er = wi < WPD - 1 ? nr : 0.f;
+    }
+    const bool ok = lane_ok && act;
+    float h[NP];
+#pragma unroll
+    for (int q = 0; q < NP; ++q) {
+      const float hl = q == 0 ? el : hp[q - 1];
+      const float hr = q == NP - 1 ? er : hp[q + 1];
+      float r = v[1].get(q) * v[0].get(q);
+      r = fmaf(v[2].get(q), hl, r);
+      r = fmaf(v[3].get(q), hp[q], r);
+      r = fmaf(v[4].get(q), hr, r);
+      h[q] = (ok && (q < VE || hi_ok)) ? r : 0.f;
+    }
+#pragma unroll
+    for (int q = 0; q < NP; ++q) hp[q] = h[q];
+    // the new h is materialised before anything below, so the refills of the
+    // ring slots land in the registers just consumed and no loop-carried copy
+    // (which would wait for the loads) is needed
+#pragma unroll
+    for (int q = 0; q < NP; ++q) asm volatile("" : "+v"(hp[q]));
+    if (lane == 0) edge[par][wave][0] = hp[0];
+    if (lane == 63) edge[par][wave][1] = hp[NP - 1];
+    if (ok) {
+      const int64_t off = (int64_t)line_of(t) * W;
+      if constexpr (SECOND) {
+        const int ka = k % RA;
+        float o[NP];
+#pragma unroll
+        for (int q = 0; q < NP; ++q) o[q] = (both ? aring[ka][q] : 0.f) + hp[q];
+        if constexpr (fin) {
+#pragma unroll
+          for (int q = 0; q < NP; ++q) o[q] *= uring[ka].get(q);
+          stv<VE>((T*)p.y + pb + off, o);
+          if (hi_ok) stv<VE>((T*)p.y + pb + off + VE, o + VE);
+        } else {
+          stv<VE>(p.acc + pb + off, o);
+          if (hi_ok) stv<VE>(p.acc + pb + off + VE, o + VE);
+        }
+      } else {
+        stv<VE>(p.acc + pb + off, hp);
+        if (hi_ok) stv<VE>(p.acc + pb + off + VE, hp + VE);
+      }
+    }
+    // refills come after the stores, which they may alias, so they stay here
+    asm volatile("" ::: "memory");
+    load_main(ring[k], s + R);
+    if constexpr (SECOND) load_aux(k % RA, s + RA);
+    lds_barrier();
+  };
+
+  // Steps [.., s1) store h (the first half of a pair, or a single direction
+  // that feeds pass H); steps [s1, nsteps) combine with the stored sum.  Idle
+  // steps before step 0 and after the last one align both loops to the ring,
+  // so every load is unconditional and stays in flight across steps.
+  constexpr bool single_final = !both && fin;
+  const int s1 = single_final ? 0 : sm;
+  const int o = (R - s1 % R) % R;
+#pragma unroll
+  for (int k = 0; k < R; ++k) load_main(ring[k], k - o);
+  for (int s0 = -o; s0 < s1; s0 += R) {
+#pragma unroll
+    for (int k = 0; k < R; ++k) step(std::false_type{}, k, s0 + k);
+  }
+  if (s1 >= nsteps) {
+    consume_ring();
+    return;
+  }
+  // the other direction's stores of the first half must be visible
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < RA; ++k) load_aux(k, s1 + k);
+  // the first turn of the ring is peeled so that the loop is entered with the
+  // loads in flight in the same order as in its steady state (otherwise the
+  // waits at its top follow the order of the preloads and drain the ring)
+#pragma unroll
+  for (int k = 0; k < R; ++k) step(std::true_type{}, k, s1 + k);
+  for (int s0 = s1 + R; s0 < nsteps; s0 += R) {
+#pragma unroll
+    for (int k = 0; k < R; ++k) step(std::true_type{}, k, s0 + k);
+  }
+  consume_ring();
+#pragma unroll
+  for (int k = 0; k < RA; ++k) {
+    if constexpr (both) {
+#pragma unroll
+      for (int q = 0; q < NP; ++q) asm volatile("" ::"v"(aring[k][q]));
+    }
+    if constexpr (fin) uring[k].pin_use();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// pass H
+// ---------------------------------------------------------------------------
+struct LargeHParams {
+  const void* x;
+  const void* lam;
+  const void* w;
+  const void* u;
+  void* y;
+  float* acc;
+  float* state;       // [2 parities][2 directions][planes][H]
+  int64_t planes, npc;
+  int H, W;
+  int slot0, slot1;   // weight slot of left-to-right / right-to-left, -1 when absent
+  int step;           // launch index
+  int nblk;           // column blocks
+  int delay;          // right-to-left starts one launch late (odd block count, both present)
+  int half;           // first launch of the second half (pairs)
+  int band_rows, nbands, halo;
+  int has_v;          // acc holds the vertical pass's partial sum
+};
+
+template <typename T, int NW>
+__global__ void __launch_bounds__(64 * NW) large_h_kernel(LargeHParams p) {
+  using C = LargeCfg<T>;
+  constexpr int K = C::KH, HV = C::HV, VE = C::VE, KP = K + 1;
+  typedef Pack<T, VE> PK;
+  extern __shared__ float lds[];  // [band_rows][KP] h of the band, then edges [2][NW][2]
+  float* edge = lds + p.band_rows * KP;
+
+  // workgroup -> (direction, plane, band); consecutive ids (the bands of a plane,
+  // which share halo rows) are placed on the same XCD
+  const int64_t G = gridDim.x, b = blockIdx.x;
+  const int64_t G8 = G / 8 * 8;
+  int64_t id = b < G8 ? (b % 8) * (G8 / 8) + b / 8 : b;
+  const int band = (int)(id % p.nbands);
+  id /= p.nbands;
+  const int64_t plane = id % p.planes;
+  const int dsel = (int)(id / p.planes);
+  const bool both = p.slot0 >= 0 && p.slot1 >= 0;
+  const int dir = both ? dsel : (p.slot0 >= 0 ? 0 : 1);  // 0: left-to-right, 1: right-to-left
+  const int slot = dir ? p.slot1 : p.slot0;
+  const int seq = dir ? p.step - p.delay : p.step;         // position in this direction's order
+  if (seq < 0 || seq >= p.nblk) return;
+  const int blk = dir ? p.nblk - 1 - seq : seq;
+  const int H = p.H, W = p.W;
+  // window of K columns: the block itself, or the last K columns for a short last block
+  const int c0 = blk * K;
+  const int ws = c0 + K <= W ? c0 : W - K;
+  const int lo = c0 - ws;  // first valid column of the window
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // lanes past the band and its halos duplicate the last row in use (no traffic)
+  const int used = p.band_rows + 2 * p.halo;
+  const int r = band * p.band_rows - p.halo + (tid < used ? tid : used - 1);
+  const bool row_ok = tid < used && r >= 0 && r < H;
+  const int rc = r < 0 ? 0 : (r >= H ? H - 1 : r);
+  const int br = tid - p.halo;  // row inside the band
+  const bool in_band = br >= 0 && br < p.band_rows && row_ok;
+
+  const int64_t HW = (int64_t)H * W;
+  const int64_t rb = plane * HW + (int64_t)rc * W + ws;
+  const T* w0 = (const T*)p.w + (int64_t)slot * 3 * p.npc;
+  const T* base[5] = {(const T*)p.x + rb, (const T*)p.lam + rb, w0 + rb, w0 + p.npc + rb,
+                      w0 + 2 * p.npc + rb};
+  // state of the previous block first: it is needed before any column
+  const int64_t sdir = (int64_t)dir * p.planes * H + plane * H;
+  float hp = 0.f;
+  if (seq > 0) {
+    const float* sin = p.state + (int64_t)((p.step - 1) & 1) * 2 * p.planes * H + sdir;
+    hp = sin[rc];
+  }
+  hp = row_ok ? hp : 0.f;
+  if (lane == 0) edge[(1 * NW + wave) * 2 + 0] = hp;
+  if (lane == 63) edge[(1 * NW + wave) * 2 + 1] = hp;
+
+  float* hrow = lds + (in_band ? br : 0) * KP;
+  auto scan = [&](auto rev_tag) __attribute__((always_inline)) {
+    constexpr bool REV = decltype(rev_tag)::value;
+    // the tile is loaded in the order its columns are used, so the first
+    // columns are computed while the rest is still arriving
+    PK tile[5][HV];
+#pragma unroll
+    for (int i = 0; i < HV; ++i) {
+      const int v = REV ? HV - 1 - i : i;
+#pragma unroll
+      for (int m = 0; m < 5; ++m) tile[m][v].load(base[m] + v * VE);
+    }
+    lds_barrier();  // initial edges published
+#pragma unroll
+  for (int i = 0; i < K; ++i) {
+    const int ti = REV ? K - 1 - i : i;  // window column of this step
+    if (ti < lo) continue;               // short last block (uniform)
+    const int par = i & 1;
+    float up = from_prev_lane(hp), dn = from_next_lane(hp);
+    if constexpr (NW > 1) {
+      const float nu = edge[((par ^ 1) * NW + (wave > 0 ? wave - 1 : wave)) * 2 + 1];
+      const float nd = edge[((par ^ 1) * NW + (wave < NW - 1 ? wave + 1 : wave)) * 2 + 0];
+      if (lane == 0) up = wave > 0 ? nu : 0.f;
+      if (lane == 63) dn = wave < NW - 1 ? nd : 0.f;
+    }
+    const float xv = tile[0][ti / VE].get(ti % VE), lv = tile[1][ti / VE].get(ti % VE);
+    const float a = tile[2][ti / VE].get(ti % VE), bw = tile[3][ti / VE].get(ti % VE),
+                cw = tile[4][ti / VE].get(ti % VE);
+    float h = lv * xv;
+    h = fmaf(a, up, h);
+    h = fmaf(bw, hp, h);
+    h = fmaf(cw, dn, h);
+    hp = row_ok ? h : 0.f;
+    if (lane == 0) edge[(par * NW + wave) * 2 + 0] = hp;
+    if (lane == 63) edge[(par * NW + wave) * 2 + 1] = hp;
+    if (in_band) hrow[ti] = hp;
+    lds_barrier();
+  }
+  };
+  if (dir) scan(std::true_type{});
+  else scan(std::false_type{});
+  if (in_band) p.state[(int64_t)(p.step & 1) * 2 * p.planes * H + sdir + r] = hp;
+  __syncthreads();
+
+  // combine the band's h with acc: y = u * (acc + h) or acc += h, 4 columns a thread
+  const bool second = both && p.step >= p.half;
+  const bool fin = !both || second;
+  const bool read_acc = second || p.has_v;
+  const int rows = min(p.band_rows, H - band * p.band_rows);
+  const int nvr = (K - lo) / 4;
+  const int n = rows * nvr;
+  const int64_t ob = plane * HW + (int64_t)band * p.band_rows * W + ws;
+  constexpr int U = 4;
+  for (int e0 = tid; e0 < n; e0 += 64 * NW * U) {
+    float av[U][4], uv[U][4];
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      const int e = e0 + k * 64 * NW < n ? e0 + k * 64 * NW : e0;
+      const int rr = e / nvr, cc = lo + (e - rr * nvr) * 4;
+      const int64_t o = ob + (int64_t)rr * W + cc;
+      if (read_acc) ldv<4>(p.acc + o, av[k]);
+      else av[k][0] = av[k][1] = av[k][2] = av[k][3] = 0.f;
+      if (fin) ldv<4>((const T*)p.u + o, uv[k]);
+    }
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      const int e = e0 + k * 64 * NW;
+      if (e < n) {
+        const int rr = e / nvr, cc = lo + (e - rr * nvr) * 4;
+        const int64_t o = ob + (int64_t)rr * W + cc;
+        float s[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) s[q] = av[k][q] + lds[rr * KP + cc + q];
+        if (fin) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) s[q] *= uv[k][q];
+          stv<4>((T*)p.y + o, s);
+        } else {
+          stv<4>(p.acc + o, s);
+        }
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// host side
+// ---------------------------------------------------------------------------
+template <typename T>
+inline bool large_fwd_supported(int H, int W) {
+  using C = LargeCfg<T>;
+  return H >= 1 && W >= C::KH && W % C::VE == 0 && W <= C::MAX_W;
+}
+
+template <typename T>
+struct LargeGeom {
+  int wpd;        // vertical: waves per direction (power of two)
+  int band_rows, nbands, halo, nw;
+  int nblk;
+  size_t lds_h;   // dynamic LDS of pass H
+};
+
+template <typename T>
+inline LargeGeom<T> large_geom(int H, int W) {
+  using C = LargeCfg<T>;
+  LargeGeom<T> g{};
+  const int need = (W + 64 * C::NPV - 1) / (64 * C::NPV);
+  g.wpd = 1;
+  while (g.wpd < need) g.wpd *= 2;
+  if (H <= C::HROWS) {
+    g.nbands = 1;
+    g.band_rows = H;
+    g.halo = 0;
+    g.nw = (H + 63) / 64;
+  } else {
+    const int core = C::HROWS - 2 * C::KH;
+    g.nbands = (H + core - 1) / core;
+    g.band_rows = (H + g.nbands - 1) / g.nbands;
+    g.halo = C::KH;
+    g.nw = (g.band_rows + 2 * C::KH + 63) / 64;
+  }
+  g.nblk = (W + C::KH - 1) / C::KH;
+  g.lds_h = ((size_t)g.band_rows * (C::KH + 1) + 2 * 8 * 2) * sizeof(float);
+  return g;
+}
+
+template <typename T, int WPD, bool BOTH, bool FIN>
+hipError_t launch_large_v_mode(const LargeVParams& p, hipStream_t st) {
+  hipLaunchKernelGGL((large_v_kernel<T, WPD, BOTH, FIN>), dim3((unsigned)p.planes),
+                     dim3((BOTH ? 128 : 64) * WPD), 0, st, p);
+  return hipGetLastError();
+}
+
+template <typename T, int WPD>
+hipError_t launch_large_v(const LargeVParams& p, bool both, hipStream_t st) {
+  if (both) return p.final_out ? launch_large_v_mode<T, WPD, true, true>(p, st)
+                               : launch_large_v_mode<T, WPD, true, false>(p, st);
+  return p.final_out ? launch_large_v_mode<T, WPD, false, true>(p, st)
+                     : launch_large_v_mode<T, WPD, false, false>(p, st);
+}
+
+template <typename T, int NW>
+hipError_t launch_large_h_nw(const LargeHParams& p, int64_t grid, size_t lds, hipStream_t st) {
+  auto kern = large_h_kernel<T, NW>;
+  if (lds > 64 * 1024) {
+    hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(64 * NW), lds, st, p);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_large_h(const LargeHParams& p, int nw, int64_t grid, size_t lds, hipStream_t st) {
+  switch (nw) {
+    case 1: return launch_large_h_nw<T, 1>(p, grid, lds, st);
+    case 2: return launch_large_h_nw<T, 2>(p, grid, lds, st);
+    case 3: return launch_large_h_nw<T, 3>(p, grid, lds, st);
+    case 4: return launch_large_h_nw<T, 4>(p, grid, lds, st);
+    case 5: return launch_large_h_nw<T, 5>(p, grid, lds, st);
+    case 6: return launch_large_h_nw<T, 6>(p, grid, lds, st);
+    case 7: return launch_large_h_nw<T, 7>(p, grid, lds, st);
+    case 8: return launch_large_h_nw<T, 8>(p, grid, lds, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <typename T>
+hipError_t large_fwd_t(const LargeFwdArgs& a) {
+  using C = LargeCfg<T>;
+  if (!large_fwd_supported<T>(a.H, a.W)) return hipErrorInvalidValue;
+  const LargeGeom<T> g = large_geom<T>(a.H, a.W);
+  hipStream_t st = (hipStream_t)a.stream;
+  const int64_t npc = a.planes * (int64_t)a.H * a.W;
+  int slot[4], n = 0;
+  for (int d = 0; d < 4; ++d) slot[d] = (a.mask >> d) & 1 ? n++ : -1;
+  const bool has_v = slot[0] >= 0 || slot[1] >= 0, has_h = slot[2] >= 0 || slot[3] >= 0;
+
+  if (has_v) {
+    LargeVParams v{};
+    v.x = a.x; v.lam = a.lam; v.w = a.w; v.u = a.u; v.y = a.y; v.acc = a.acc;
+    v.planes = a.planes; v.npc = npc; v.H = a.H; v.W = a.W;
+    v.slot0 = slot[0]; v.slot1 = slot[1];
+    v.final_out = has_h ? 0 : 1;
+    const bool both = slot[0] >= 0 && slot[1] >= 0;
+    hipError_t e;
+    switch (g.wpd) {
+      case 1: e = launch_large_v<T, 1>(v, both, st); break;
+      case 2: e = launch_large_v<T, 2>(v, both, st); break;
+      case 4: e = launch_large_v<T, 4>(v, both, st); break;
+      default: e = hipErrorInvalidValue;
+    }
+    if (e != hipSuccess) return e;
+  }
+  if (!has_h) return hipSuccess;
+  LargeHParams h{};
+  h.x = a.x; h.lam = a.lam; h.w = a.w; h.u = a.u; h.y = a.y; h.acc = a.acc; h.state = a.state;
+  h.planes = a.planes; h.npc = npc; h.H = a.H; h.W = a.W;
+  h.slot0 = slot[2]; h.slot1 = slot[3];
+  const bool both = slot[2] >= 0 && slot[3] >= 0;
+  h.nblk = g.nblk;
+  h.delay = both ? (g.nblk & 1) : 0;
+  h.half = both ? g.nblk / 2 + h.delay : 0;
+  h.band_rows = g.band_rows; h.nbands = g.nbands; h.halo = g.halo;
+  h.has_v = has_v ? 1 : 0;
+  const int64_t grid = (int64_t)g.nbands * a.planes * (both ? 2 : 1);
+  if (grid > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+  for (int j = 0; j < g.nblk + h.delay; ++j) {
+    h.step = j;
+    hipError_t e = launch_large_h<T>(h, g.nw, grid, g.lds_h, st);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+}  // namespace gspn

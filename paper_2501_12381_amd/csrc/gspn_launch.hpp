@@ -111,4 +111,25 @@ inline hipError_t resident_bwd(const ResidentBwdArgs& a) {
 }
 bool resident_fits(int H, int W, int dtype, bool backward);
 
+// ---- two-pass family: planes too large for LDS -------------------------------
+struct LargeFwdArgs {
+  const void* x;
+  const void* lam;
+  const void* w;   // all n directions, packed [n][3][B][C][H][W]
+  const void* u;
+  void* y;
+  float* acc;      // fp32 partial sums, B*C*H*W (needed when n > 1)
+  float* state;    // 2 * 2 * B*C*H floats (needed with a horizontal direction)
+  uint32_t mask;
+  int64_t planes;
+  int H, W, dtype;
+  void* stream;
+};
+hipError_t large_fwd_f32(const LargeFwdArgs& a);
+hipError_t large_fwd_bf16(const LargeFwdArgs& a);
+inline hipError_t large_fwd(const LargeFwdArgs& a) {
+  return a.dtype == 0 ? large_fwd_f32(a) : large_fwd_bf16(a);
+}
+bool large_fwd_fits(int H, int W, int dtype);
+
 }  // namespace gspn

@@ -44,7 +44,7 @@ def test_header_constants_match_binding():
     consts = dict(re.findall(r"\b(GSPN_[A-Z0-9_]+)\s*=\s*(\d+)u?", src))
     for name in ("GSPN_F32", "GSPN_BF16", "GSPN_DIR_T2B", "GSPN_DIR_B2T", "GSPN_DIR_L2R",
                  "GSPN_DIR_R2L", "GSPN_ALGO_AUTO", "GSPN_ALGO_RESIDENT", "GSPN_ALGO_STREAM",
-                 "GSPN_ALGO_RESIDENT_GENERIC"):
+                 "GSPN_ALGO_RESIDENT_GENERIC", "GSPN_ALGO_TWO_PASS"):
         assert int(consts[name]) == getattr(L, name), name
     for code, name in L.STATUS.items():
         assert int(consts[name]) == code, name
@@ -69,6 +69,21 @@ def test_workspace_sizes():
     assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 7, 0xF, bf, S) % 256 == 0
     # streaming backward: previous-line state, sum of h, sum of g (fp32 each)
     assert L.gspn_scan_bwd_workspace_bytes(2, 3, 5, 7, 0xF, f32, S) >= 3 * npc * 4
+    # two-pass forward: fp32 partial sums (several directions), then the column
+    # state of the horizontal pass (2 parities x 2 directions x planes x H floats)
+    T = L.GSPN_ALGO_TWO_PASS
+    acc, state = 2 * 3 * 5 * 64 * 4, 512  # 7680 is a multiple of 256; 4*6*5*4 = 480 -> 512
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 64, 0xF, bf, T) == acc + state
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 64, 0x3, bf, T) == acc
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 64, 0x4, bf, T) == state
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 64, 0x1, bf, T) == 0
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 60, 0xF, bf, T) == 0  # W*2 not a multiple of 16
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 56, 0xF, bf, T) == 0  # row under 128 bytes
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 32, 0xF, f32, T) == 2 * 3 * 5 * 32 * 4 + 512
+    assert L.gspn_scan_bwd_workspace_bytes(2, 3, 5, 64, 0xF, bf, T) == 0  # forward only
+    # AUTO takes the two-pass kernels for planes that do not fit on chip
+    big = L.gspn_scan_fwd_workspace_bytes(1, 2, 2048, 2048, 0xF, bf, L.GSPN_ALGO_AUTO)
+    assert big == 2 * 2048 * 2048 * 4 + 4 * 2 * 2048 * 4
     # invalid problems report 0
     assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 7, 0, f32, S) == 0
     assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 7, 1, 7, S) == 0
@@ -115,6 +130,9 @@ def test_fwd_rejects_bad_arguments(lib):
     assert fwd(ws=FAKE + (5 << 30) + 64) == 5  # workspace must be 256-byte aligned
     assert fwd(ws=FAKE + 256) == 6  # workspace overlaps x (x spans 512 bytes)
     assert fwd(algo=L.GSPN_ALGO_RESIDENT, H=4096, W=4096) == 7
+    assert fwd(algo=L.GSPN_ALGO_TWO_PASS) == 7  # 8 fp32 columns: row under 128 bytes
+    # the two-pass kernels need 16-byte aligned tensors when forced
+    assert fwd(algo=L.GSPN_ALGO_TWO_PASS, W=64, dtype=L.GSPN_BF16, x=FAKE + 2) == 5
 
 
 def test_empty_problem_is_a_noop(lib):

@@ -11,16 +11,18 @@ from tests.parity_util import TOL, assert_close, np64, oracle_fwd
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
-ALGOS = [L.GSPN_ALGO_AUTO, L.GSPN_ALGO_STREAM, L.GSPN_ALGO_RESIDENT, L.GSPN_ALGO_RESIDENT_GENERIC]
-ALGO_NAMES = {0: "auto", 1: "resident", 2: "stream", 3: "resident_generic"}
+ALGOS = [L.GSPN_ALGO_AUTO, L.GSPN_ALGO_STREAM, L.GSPN_ALGO_RESIDENT, L.GSPN_ALGO_RESIDENT_GENERIC,
+         L.GSPN_ALGO_TWO_PASS]
+ALGO_NAMES = {0: "auto", 1: "resident", 2: "stream", 3: "resident_generic", 4: "two_pass"}
+FORCED = (L.GSPN_ALGO_RESIDENT, L.GSPN_ALGO_RESIDENT_GENERIC, L.GSPN_ALGO_TWO_PASS)
 
 
 def run_fwd(inp, mask, algo):
     try:
         return ops.gspn_scan_fwd(inp["x"], inp["w"], inp["lam"], inp["u"], mask, algo=algo)
     except L.GSPNError as e:
-        if e.status == 7 and algo in (L.GSPN_ALGO_RESIDENT, L.GSPN_ALGO_RESIDENT_GENERIC):
-            pytest.skip("resident kernel does not take this shape")
+        if e.status == 7 and algo in FORCED:
+            pytest.skip(f"{ALGO_NAMES[algo]} kernels do not take this shape")
         raise
 
 
@@ -74,6 +76,56 @@ def test_edge_shapes_all_directions(shape, dtype, algo):
     y = run_fwd(inp, 0xF, algo)
     torch.cuda.synchronize()
     assert_close(y, oracle_fwd(inp, 0xF), dtype, f"{H}x{W}")
+
+
+# Two-pass family: single and several row bands (halo rows), odd line counts
+# (middle-line rule), ragged and odd numbers of column blocks, rows spread over
+# one to four waves per direction.
+TWO_PASS_SHAPES = [(1, 64), (2, 64), (3, 72), (71, 136), (130, 200), (600, 64), (1000, 40),
+                   (1100, 96), (520, 1032), (33, 2056)]
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16], ids=["f32", "bf16"])
+@pytest.mark.parametrize("shape", TWO_PASS_SHAPES, ids=lambda s: f"{s[0]}x{s[1]}")
+def test_two_pass_shapes(shape, dtype):
+    H, W = shape
+    print(f"[fwd] two-pass {H}x{W} {dtype}", flush=True)
+    inp = general_inputs(1, 2, H, W, 0xF, dtype, seed=H * 7919 + W)
+    y = run_fwd(inp, 0xF, L.GSPN_ALGO_TWO_PASS)
+    torch.cuda.synchronize()
+    assert_close(y, oracle_fwd(inp, 0xF), dtype, f"{H}x{W}")
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16], ids=["f32", "bf16"])
+@pytest.mark.parametrize("mask", list(range(1, 16)))
+def test_two_pass_every_mask(mask, dtype):
+    H, W = 67, 136  # odd H, three column blocks in bf16 (the last one short)
+    print(f"[fwd] two-pass mask {mask} {dtype}", flush=True)
+    inp = general_inputs(2, 2, H, W, mask, dtype, seed=100 + mask)
+    y = run_fwd(inp, mask, L.GSPN_ALGO_TWO_PASS)
+    torch.cuda.synchronize()
+    assert_close(y, oracle_fwd(inp, mask), dtype, f"mask {mask}")
+
+
+def test_two_pass_deterministic_and_closed_form():
+    H, W = 130, 200
+    inp = general_inputs(1, 3, H, W, 0xF, torch.bfloat16, seed=3)
+    a = run_fwd(inp, 0xF, L.GSPN_ALGO_TWO_PASS)
+    b = run_fwd(inp, 0xF, L.GSPN_ALGO_TWO_PASS)
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    # middle weight 1: each direction is a cumulative sum of lam*x
+    g = torch.Generator(device=DEV).manual_seed(8)
+    x = torch.randn(1, 2, 600, 64, device=DEV, generator=g)
+    lam = torch.rand(1, 2, 600, 64, device=DEV, generator=g)
+    u = torch.ones_like(x)
+    lx = np64(lam * x)
+    for d, axis, rev in ((1, 2, False), (2, 2, True), (4, 3, False), (8, 3, True)):
+        w = torch.zeros(1, 3, 1, 2, 600, 64, device=DEV)
+        w[:, 1] = 1.0
+        y = run_fwd(dict(x=x, lam=lam, u=u, w=w), d, L.GSPN_ALGO_TWO_PASS)
+        ref = np.flip(np.cumsum(np.flip(lx, axis), axis), axis) if rev else np.cumsum(lx, axis)
+        assert_close(y, ref, torch.float32, f"dir {d}")
 
 
 @pytest.mark.parametrize("algo", ALGOS, ids=lambda a: ALGO_NAMES[a])
