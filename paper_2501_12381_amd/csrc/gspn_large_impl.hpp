@@ -48,27 +48,6 @@ struct LargeCfg {
   static constexpr int MAX_W = MAX_WPD * 64 * NPV; // widest row of the vertical pass
 };
 
-// Two 16-byte vectors of a lane: positions [0, VE) at p, [VE, 2 VE) at p + hoff
-// (hoff = 0 re-reads the first vector when the row ends after it).
-template <typename T>
-struct Pack2 {
-  static constexpr int VE = LargeCfg<T>::VE;
-  static constexpr int kWords = 2 * Pack<T, VE>::kWords;
-  Pack<T, VE> a, b;
-  __device__ __forceinline__ void load(const T* __restrict__ p, int hoff) {
-    a.load(p);
-    b.load(p + hoff);
-  }
-  __device__ __forceinline__ float get(int q) const { return q < VE ? a.get(q) : b.get(q - VE); }
-  __device__ __forceinline__ void pin_use() const {
-#pragma unroll
-    for (int i = 0; i < Pack<T, VE>::kWords; ++i) {
-      asm volatile("" ::"v"(a.w[i]));
-      asm volatile("" ::"v"(b.w[i]));
-    }
-  }
-};
-
 // ---------------------------------------------------------------------------
 // pass V
 // ---------------------------------------------------------------------------
@@ -85,15 +64,23 @@ struct LargeVParams {
   int final_out;     // nonzero: write y = u * sum; zero: write the fp32 partial sum
 };
 
-// BOTH: both vertical directions are present; FIN: write y (no pass H follows)
+// Layout of a row over a wave: the wave's span of 64 * NP positions is cut into
+// NQ chunks of 64 * G positions; lane l holds positions [l G, l G + G) of every
+// chunk.  Each load or store instruction then covers one chunk: consecutive
+// lanes, consecutive addresses, whole cache lines (bf16 and fp32 alike).  The
+// left neighbour of a chunk's first position is lane 63's last one of the
+// previous chunk (a lane read), of the previous wave (LDS) or padding.
+//
+// BOTH: both vertical directions are present; FIN: write y (no pass H follows).
 template <typename T, int WPD, bool BOTH, bool FIN>
 __global__ void __launch_bounds__(128 * WPD, 2) large_v_kernel(LargeVParams p) {
   using C = LargeCfg<T>;
   constexpr int NP = C::NPV, R = C::RV, RA = C::RA;
   static_assert(R % RA == 0, "acc ring slots must repeat with the input ring");
-  constexpr int VE = C::VE;
-  typedef Pack2<T> PK;
-  static_assert(NP == 2 * VE, "a lane holds two 16-byte vectors");
+  constexpr int G = 4;           // positions per lane and chunk
+  constexpr int NQ = NP / G;     // chunks per wave span
+  constexpr int SPAN = 64 * G;   // positions per chunk
+  typedef Pack<T, G> PK;
   __shared__ float edge[2][2 * WPD][2];  // [step parity][wave][first, last position]
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -102,11 +89,16 @@ __global__ void __launch_bounds__(128 * WPD, 2) large_v_kernel(LargeVParams p) {
   const int wi = both ? wave - dir * WPD : wave;
   const int64_t plane = blockIdx.x;
   const int H = p.H, W = p.W;
-  const int pos0 = (wi * 64 + lane) * NP;
-  const bool lane_ok = pos0 < W;
-  const bool hi_ok = pos0 + VE < W;              // the lane's second vector is in the row
-  const int hoff = hi_ok ? VE : 0;
-  const int64_t pb = plane * (int64_t)H * W + (lane_ok ? pos0 : 0);
+  // per chunk: position of the lane's first element, whether it is in the row
+  int po[NQ];
+  bool qok[NQ];
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    const int pos = wi * NQ * SPAN + q * SPAN + lane * G;
+    qok[q] = pos < W;  // W is a multiple of G
+    po[q] = qok[q] ? pos : 0;
+  }
+  const int64_t pb = plane * (int64_t)H * W;
   const int slot = dir ? p.slot1 : p.slot0;
   const int odd = both ? (H & 1) : 0;
   const int nsteps = H + odd;
@@ -128,93 +120,124 @@ __global__ void __launch_bounds__(128 * WPD, 2) large_v_kernel(LargeVParams p) {
     return dir ? H - 1 - t : t;
   };
 
-  PK ring[R][5];
+  PK ring[R][5][NQ];
   // Keeps the last prefetches "used" after a loop: without a use the compiler
   // drains every outstanding load at the top of each iteration.
   auto consume_ring = [&]() __attribute__((always_inline)) {
 #pragma unroll
     for (int k = 0; k < R; ++k)
 #pragma unroll
-      for (int m = 0; m < 5; ++m) ring[k][m].pin_use();
+      for (int m = 0; m < 5; ++m)
+#pragma unroll
+        for (int q = 0; q < NQ; ++q)
+#pragma unroll
+          for (int i = 0; i < PK::kWords; ++i) asm volatile("" ::"v"(ring[k][m][q].w[i]));
   };
-  auto load_main = [&](PK (&sl)[5], int s) __attribute__((always_inline)) {
+  auto load_main = [&](PK (&sl)[5][NQ], int s) __attribute__((always_inline)) {
     const int64_t off = (int64_t)line_of(t_of(s)) * W;
 #pragma unroll
-    for (int m = 0; m < 5; ++m) sl[m].load(base[m] + off, hoff);
+    for (int m = 0; m < 5; ++m)
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) sl[m][q].load(base[m] + off + po[q]);
   };
   // second-half (or final single-direction) operands: acc and u of the step's row
-  PK uring[RA];
-  float aring[RA][NP];
+  PK uring[RA][NQ];
+  float aring[RA][NQ][G];
   auto load_aux = [&](int k, int s) __attribute__((always_inline)) {
     const int64_t off = (int64_t)line_of(t_of(s)) * W;
-    if constexpr (fin) uring[k].load(ubase + off, hoff);
-    if constexpr (both) {
-      ldv<VE>(abase + off, aring[k]);
-      ldv<VE>(abase + off + hoff, aring[k] + VE);
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      if constexpr (fin) uring[k][q].load(ubase + off + po[q]);
+      if constexpr (both) ldv<G>(abase + off + po[q], aring[k][q]);
     }
   };
 
-  float hp[NP];
+  float hp[NQ][G];
 #pragma unroll
-  for (int q = 0; q < NP; ++q) hp[q] = 0.f;
-
+  for (int q = 0; q < NQ; ++q)
+#pragma unroll
+    for (int j = 0; j < G; ++j) hp[q][j] = 0.f;
 
   // one step of the scan; SECOND: combine with the other direction's stored h
   auto step = [&](auto second_tag, int k, int s) __attribute__((always_inline)) {
     constexpr bool SECOND = decltype(second_tag)::value;
-    const PK(&v)[5] = ring[k];  // unpacked at use; the slot is refilled after the step
+    const PK(&v)[5][NQ] = ring[k];  // unpacked at use; the slot is refilled after the step
     const int t = t_of(s);
     const bool act = t >= 0 && t < H;
     const int par = s & 1;
-    // neighbours of the lane's first and last position on the previous row
-    float el = from_prev_lane(hp[NP - 1]);
-    float er = from_next_lane(hp[0]);
+    // neighbours of each chunk's first and last position on the previous row
+    float el[NQ], er[NQ];
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      el[q] = from_prev_lane(hp[q][G - 1]);
+      er[q] = from_next_lane(hp[q][0]);
+    }
+    float wl = 0.f, wr = 0.f;  // across waves
     if constexpr (WPD > 1) {
       const float nl = edge[par ^ 1][wi > 0 ? wave - 1 : wave][1];
       const float nr = edge[par ^ 1][wi < WPD - 1 ? wave + 1 : wave][0];
-      if (lane == 0) el = wi > 0 ? nl : 0.f;
-      if (lane == 63) er = wi < WPD - 1 ? nr : 0.f;
-    }
-    const bool ok = lane_ok && act;
-    float h[NP];
-#pragma unroll
-    for (int q = 0; q < NP; ++q) {
-      const float hl = q == 0 ? el : hp[q - 1];
-      const float hr = q == NP - 1 ? er : hp[q + 1];
-      float r = v[1].get(q) * v[0].get(q);
-      r = fmaf(v[2].get(q), hl, r);
-      r = fmaf(v[3].get(q), hp[q], r);
-      r = fmaf(v[4].get(q), hr, r);
-      h[q] = (ok && (q < VE || hi_ok)) ? r : 0.f;
+      wl = wi > 0 ? nl : 0.f;
+      wr = wi < WPD - 1 ? nr : 0.f;
     }
 #pragma unroll
-    for (int q = 0; q < NP; ++q) hp[q] = h[q];
+    for (int q = 0; q < NQ; ++q) {
+      const float pl = q > 0 ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(
+                                                              __builtin_bit_cast(int, hp[q - 1][G - 1]), 63))
+                             : wl;
+      const float nr = q < NQ - 1 ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(
+                                                                   __builtin_bit_cast(int, hp[q + 1][0]), 0))
+                                  : wr;
+      if (lane == 0) el[q] = pl;
+      if (lane == 63) er[q] = nr;
+    }
+    float h[NQ][G];
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const bool ok = qok[q] && act;
+#pragma unroll
+      for (int j = 0; j < G; ++j) {
+        const float hl = j == 0 ? el[q] : hp[q][j - 1];
+        const float hr = j == G - 1 ? er[q] : hp[q][j + 1];
+        float r = v[1][q].get(j) * v[0][q].get(j);
+        r = fmaf(v[2][q].get(j), hl, r);
+        r = fmaf(v[3][q].get(j), hp[q][j], r);
+        r = fmaf(v[4][q].get(j), hr, r);
+        h[q][j] = ok ? r : 0.f;
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < NQ; ++q)
+#pragma unroll
+      for (int j = 0; j < G; ++j) hp[q][j] = h[q][j];
     // the new h is materialised before anything below, so the refills of the
     // ring slots land in the registers just consumed and no loop-carried copy
     // (which would wait for the loads) is needed
 #pragma unroll
-    for (int q = 0; q < NP; ++q) asm volatile("" : "+v"(hp[q]));
-    if (lane == 0) edge[par][wave][0] = hp[0];
-    if (lane == 63) edge[par][wave][1] = hp[NP - 1];
-    if (ok) {
+    for (int q = 0; q < NQ; ++q)
+#pragma unroll
+      for (int j = 0; j < G; ++j) asm volatile("" : "+v"(hp[q][j]));
+    if (lane == 0) edge[par][wave][0] = hp[0][0];
+    if (lane == 63) edge[par][wave][1] = hp[NQ - 1][G - 1];
+    if (act) {
       const int64_t off = (int64_t)line_of(t) * W;
-      if constexpr (SECOND) {
-        const int ka = k % RA;
-        float o[NP];
 #pragma unroll
-        for (int q = 0; q < NP; ++q) o[q] = (both ? aring[ka][q] : 0.f) + hp[q];
-        if constexpr (fin) {
+      for (int q = 0; q < NQ; ++q) {
+        if (!qok[q]) continue;
+        if constexpr (SECOND) {
+          const int ka = k % RA;
+          float o[G];
 #pragma unroll
-          for (int q = 0; q < NP; ++q) o[q] *= uring[ka].get(q);
-          stv<VE>((T*)p.y + pb + off, o);
-          if (hi_ok) stv<VE>((T*)p.y + pb + off + VE, o + VE);
+          for (int j = 0; j < G; ++j) o[j] = (both ? aring[ka][q][j] : 0.f) + hp[q][j];
+          if constexpr (fin) {
+#pragma unroll
+            for (int j = 0; j < G; ++j) o[j] *= uring[ka][q].get(j);
+            stv<G>((T*)p.y + pb + off + po[q], o);
+          } else {
+            stv<G>(p.acc + pb + off + po[q], o);
+          }
         } else {
-          stv<VE>(p.acc + pb + off, o);
-          if (hi_ok) stv<VE>(p.acc + pb + off + VE, o + VE);
+          stv<G>(p.acc + pb + off + po[q], hp[q]);
         }
-      } else {
-        stv<VE>(p.acc + pb + off, hp);
-        if (hi_ok) stv<VE>(p.acc + pb + off + VE, hp + VE);
       }
     }
     // refills come after the stores, which they may alias, so they stay here
@@ -256,13 +279,18 @@ __global__ void __launch_bounds__(128 * WPD, 2) large_v_kernel(LargeVParams p) {
   }
   consume_ring();
 #pragma unroll
-  for (int k = 0; k < RA; ++k) {
-    if constexpr (both) {
+  for (int k = 0; k < RA; ++k)
 #pragma unroll
-      for (int q = 0; q < NP; ++q) asm volatile("" ::"v"(aring[k][q]));
+    for (int q = 0; q < NQ; ++q) {
+      if constexpr (both) {
+#pragma unroll
+        for (int j = 0; j < G; ++j) asm volatile("" ::"v"(aring[k][q][j]));
+      }
+      if constexpr (fin) {
+#pragma unroll
+        for (int i = 0; i < PK::kWords; ++i) asm volatile("" ::"v"(uring[k][q].w[i]));
+      }
     }
-    if constexpr (fin) uring[k].pin_use();
-  }
 }
 
 // ---------------------------------------------------------------------------
@@ -347,11 +375,13 @@ __global__ void __launch_bounds__(64 * NW) large_h_kernel(LargeHParams p) {
     // the tile is loaded in the order its columns are used, so the first
     // columns are computed while the rest is still arriving
     PK tile[5][HV];
+    // (scheduling barriers keep this issue order)
 #pragma unroll
     for (int i = 0; i < HV; ++i) {
       const int v = REV ? HV - 1 - i : i;
 #pragma unroll
       for (int m = 0; m < 5; ++m) tile[m][v].load(base[m] + v * VE);
+      __builtin_amdgcn_sched_barrier(0);
     }
     lds_barrier();  // initial edges published
 #pragma unroll
@@ -385,41 +415,44 @@ __global__ void __launch_bounds__(64 * NW) large_h_kernel(LargeHParams p) {
   if (in_band) p.state[(int64_t)(p.step & 1) * 2 * p.planes * H + sdir + r] = hp;
   __syncthreads();
 
-  // combine the band's h with acc: y = u * (acc + h) or acc += h, 4 columns a thread
+  // combine the band's h with acc: y = u * (acc + h) or acc + h, one 16-byte
+  // vector of T (VE columns) a thread; all loads of a thread are issued before
+  // any is used, so the epilogue waits for memory once
   const bool second = both && p.step >= p.half;
   const bool fin = !both || second;
   const bool read_acc = second || p.has_v;
   const int rows = min(p.band_rows, H - band * p.band_rows);
-  const int nvr = (K - lo) / 4;
+  const int nvr = (K - lo) / VE;
   const int n = rows * nvr;
   const int64_t ob = plane * HW + (int64_t)band * p.band_rows * W + ws;
-  constexpr int U = 4;
+  constexpr int U = (C::HROWS * (K / VE) + 64 * NW - 1) / (64 * NW) < 8
+                        ? (C::HROWS * (K / VE) + 64 * NW - 1) / (64 * NW) : 8;
   for (int e0 = tid; e0 < n; e0 += 64 * NW * U) {
-    float av[U][4], uv[U][4];
+    float av[U][VE];
+    Pack<T, VE> uv[U];
 #pragma unroll
     for (int k = 0; k < U; ++k) {
       const int e = e0 + k * 64 * NW < n ? e0 + k * 64 * NW : e0;
-      const int rr = e / nvr, cc = lo + (e - rr * nvr) * 4;
+      const int rr = e / nvr, cc = lo + (e - rr * nvr) * VE;
       const int64_t o = ob + (int64_t)rr * W + cc;
-      if (read_acc) ldv<4>(p.acc + o, av[k]);
-      else av[k][0] = av[k][1] = av[k][2] = av[k][3] = 0.f;
-      if (fin) ldv<4>((const T*)p.u + o, uv[k]);
+      if (read_acc) ldv<VE>(p.acc + o, av[k]);
+      if (fin) uv[k].load((const T*)p.u + o);
     }
 #pragma unroll
     for (int k = 0; k < U; ++k) {
       const int e = e0 + k * 64 * NW;
       if (e < n) {
-        const int rr = e / nvr, cc = lo + (e - rr * nvr) * 4;
+        const int rr = e / nvr, cc = lo + (e - rr * nvr) * VE;
         const int64_t o = ob + (int64_t)rr * W + cc;
-        float s[4];
+        float s[VE];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) s[q] = av[k][q] + lds[rr * KP + cc + q];
+        for (int q = 0; q < VE; ++q) s[q] = (read_acc ? av[k][q] : 0.f) + lds[rr * KP + cc + q];
         if (fin) {
 #pragma unroll
-          for (int q = 0; q < 4; ++q) s[q] *= uv[k][q];
-          stv<4>((T*)p.y + o, s);
+          for (int q = 0; q < VE; ++q) s[q] *= uv[k].get(q);
+          stv<VE>((T*)p.y + o, s);
         } else {
-          stv<4>(p.acc + o, s);
+          stv<VE>(p.acc + o, s);
         }
       }
     }
