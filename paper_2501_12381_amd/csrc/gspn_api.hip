@@ -255,6 +255,7 @@ int gspn_scan_bwd(const void* dy, const void* x, const void* w, const void* lam,
     r.dy = dy; r.x = x; r.lam = lam; r.w = w; r.u = u;
     r.dx = dx; r.dw = dw; r.dlam = dlam; r.du = du;
     r.mask = mask; r.planes = p.planes; r.H = (int)H; r.W = (int)W; r.dtype = dtype;
+    r.use_staged = a == GSPN_ALGO_RESIDENT;
     r.stream = stream;
     return hip_status(resident_bwd(r));
   }

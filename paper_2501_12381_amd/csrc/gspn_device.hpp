@@ -14,9 +14,12 @@ typedef __bf16 bf16;
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ float bf_lo(uint32_t v) { return __uint_as_float(v << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t v) { return __uint_as_float(v & 0xffff0000u); }
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+// two floats -> two bf16 in one word (a in the low half), one packed convert
 __device__ __forceinline__ uint32_t pack_bf2(float a, float b) {
-  bf16 lo = (bf16)a, hi = (bf16)b;
-  return (uint32_t)__builtin_bit_cast(uint16_t, lo) | ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
+  const f32x2_t v = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
 }
 
 __device__ __forceinline__ float to_f(float v) { return v; }
@@ -89,17 +92,18 @@ template <int N> __device__ __forceinline__ void stv(bf16* __restrict__ p, const
 }
 
 // ---------------------------------------------------------------------------
-// cross-lane moves inside a wave64 (DPP wave shifts; all 64 lanes must be active)
+// cross-lane moves inside a wave64 (DPP wave shifts with the bound control set,
+// so the lane without a source reads zero; all 64 lanes must be active)
 // ---------------------------------------------------------------------------
 // lane l receives lane l-1's value; lane 0 receives 0
 __device__ __forceinline__ float from_prev_lane(float v) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v),
-                                                               0x138 /* wave_shr:1 */, 0xf, 0xf, false));
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x138 /* wave_shr:1 */,
+                                                            0xf, 0xf, true));
 }
 // lane l receives lane l+1's value; lane 63 receives 0
 __device__ __forceinline__ float from_next_lane(float v) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v),
-                                                               0x130 /* wave_shl:1 */, 0xf, 0xf, false));
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x130 /* wave_shl:1 */,
+                                                            0xf, 0xf, true));
 }
 
 // Workgroup barrier that orders LDS accesses only: waits for this wave's LDS

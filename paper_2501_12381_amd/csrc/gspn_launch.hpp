@@ -102,6 +102,7 @@ struct ResidentBwdArgs {
   uint32_t mask;
   int64_t planes;
   int H, W, dtype;
+  int use_staged;  // allow the LDS-staged kernel for small planes
   void* stream;
 };
 hipError_t resident_bwd_f32(const ResidentBwdArgs& a);

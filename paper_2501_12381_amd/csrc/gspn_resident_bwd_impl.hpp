@@ -60,6 +60,7 @@ struct ResBwdParams {
   int64_t npc;
   int64_t planes;
   int slot[4];
+  int nd;   // directions present
   int vec;  // 16-byte vectors legal for the elementwise passes
 };
 
@@ -302,29 +303,6 @@ hipError_t launch_resident_bwd(const ResBwdParams& p, hipStream_t st) {
   const int64_t groups = (p.planes + C::PPW - 1) / C::PPW;
   hipLaunchKernelGGL(kern, dim3((unsigned)groups), dim3(256), C::LDS_BYTES, st, p);
   return hipGetLastError();
-}
-
-template <typename T>
-hipError_t resident_bwd_t(const ResidentBwdArgs& a) {
-  ResBwdParams p;
-  p.dy = a.dy; p.x = a.x; p.lam = a.lam; p.w = a.w; p.u = a.u;
-  p.dx = a.dx; p.dw = a.dw; p.dlam = a.dlam; p.du = a.du;
-  p.planes = a.planes;
-  p.npc = (int64_t)a.planes * a.H * a.W;
-  int n = 0;
-  for (int d = 0; d < 4; ++d) p.slot[d] = (a.mask >> d) & 1 ? n++ : -1;
-  auto al16 = [](const void* q) { return ((uintptr_t)q % 16) == 0; };
-  p.vec = al16(a.dy) && al16(a.x) && al16(a.lam) && al16(a.u) && al16(a.dx) && al16(a.dlam) && al16(a.du);
-  const bool ok = al16(a.x) && al16(a.lam) && al16(a.w) && al16(a.u) && al16(a.dy) && al16(a.dw);
-  if (!ok || !resident_bwd_size_supported(a.H, a.W)) return hipErrorInvalidValue;
-  hipStream_t st = (hipStream_t)a.stream;
-  switch (a.H) {
-    case 16: return launch_resident_bwd<T, 16>(p, st);
-    case 28: return launch_resident_bwd<T, 28>(p, st);
-    case 32: return launch_resident_bwd<T, 32>(p, st);
-    case 56: return launch_resident_bwd<T, 56>(p, st);
-    default: return launch_resident_bwd<T, 64>(p, st);
-  }
 }
 
 }  // namespace gspn

@@ -1,7 +1,7 @@
 // Resident-family kernels instantiated for fp32 storage.
 #include "gspn_resident_impl.hpp"
 #include "gspn_fixed_impl.hpp"
-#include "gspn_resident_bwd_impl.hpp"
+#include "gspn_staged_bwd_impl.hpp"
 
 namespace gspn {
 hipError_t resident_fwd_f32(const ResidentFwdArgs& a) { return resident_fwd_t<float>(a); }

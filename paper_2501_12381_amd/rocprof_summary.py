@@ -2,7 +2,10 @@
 
     python -m paper_2501_12381_amd.rocprof_summary stats DIR
     python -m paper_2501_12381_amd.rocprof_summary traffic FETCH_DIR WRITE_DIR --copy-bytes N \
-        --workload NAME --kernel-map gspn_scan_bwd=resident_bwd_kernel [...] [--json OUT]
+        --workload NAME --kernel-map gspn_scan_bwd=resident_bwd_kernel [...] [--calls K] [--json OUT]
+
+`counters DIR --kernel PATTERN` prints the mean per-dispatch value of every
+counter collected for the kernels whose name contains PATTERN.
 
 `stats` prints per-kernel call count and average/min/max duration from a
 `rocprofv3 --kernel-trace --stats --output-format csv` run.
@@ -11,7 +14,10 @@
 reported in KiB per dispatch) into HBM bytes per launch.  Each counter is
 scaled by the factor that makes it read the known byte count of the plain copy
 kernel the benchmark runs for calibration (`--copy-bytes` read and written),
-so the result is in the same units as the algorithmic bytes.
+so the result is in the same units as the algorithmic bytes.  With `--calls K`
+the bytes of all dispatches matching a pattern are summed and divided by K:
+the traffic of one API call that launches several kernels (the two-pass
+forward), when the profiled run made K such calls.
 """
 from __future__ import annotations
 
@@ -72,6 +78,19 @@ def counter_values(d: str, counter: str) -> dict:
     return {k: list(v.values()) for k, v in vals.items()}
 
 
+def all_counters(d: str, pattern: str) -> dict:
+    """counter name -> mean per-dispatch value over the kernels whose name contains pattern."""
+    vals = defaultdict(lambda: defaultdict(float))
+    for path in _find(d, "counter_collection.csv"):
+        for row in csv.DictReader(open(path)):
+            if pattern not in _col(row, "Kernel_Name", "KernelName"):
+                continue
+            disp = _col(row, "Dispatch_Id", "DispatchId", "Correlation_Id")
+            vals[_col(row, "Counter_Name", "CounterName")][disp] += float(
+                _col(row, "Counter_Value", "CounterValue", "Value"))
+    return {k: sum(v.values()) / len(v) for k, v in vals.items()}
+
+
 def short(name: str, width: int = 90) -> str:
     return name if len(name) <= width else name[: width - 3] + "..."
 
@@ -115,11 +134,13 @@ def cmd_traffic(args) -> int:
         if not f or not w:
             print(f"{call}: kernel matching {pattern!r} not found", file=sys.stderr)
             return 1
-        fb = sum(f) / len(f) * 1024.0 * sf
-        wb = sum(w) / len(w) * 1024.0 * sw
+        div_f, div_w = (args.calls, args.calls) if args.calls else (len(f), len(w))
+        fb = sum(f) / div_f * 1024.0 * sf
+        wb = sum(w) / div_w * 1024.0 * sw
         result["kernels"][call] = {"kernel": pattern, "fetch_bytes_per_launch": fb,
                                    "write_bytes_per_launch": wb,
-                                   "hbm_bytes_per_launch": fb + wb}
+                                   "hbm_bytes_per_launch": fb + wb,
+                                   "dispatches": len(f), "calls": args.calls or len(f)}
         print(f"{call} ({pattern}): fetch {fb / 1e6:.1f} MB + write {wb / 1e6:.1f} MB "
               f"= {(fb + wb) / 1e6:.1f} MB per launch")
     if args.json:
@@ -127,6 +148,16 @@ def cmd_traffic(args) -> int:
             result["kernel_source_hash"] = args.source_hash
         with open(args.json, "w") as fh:
             json.dump(result, fh, indent=1)
+    return 0
+
+
+def cmd_counters(args) -> int:
+    vals = all_counters(args.dir, args.kernel)
+    if not vals:
+        print(f"no counters for kernels matching {args.kernel!r} under {args.dir}", file=sys.stderr)
+        return 1
+    for k in sorted(vals):
+        print(f"{k:32s} {vals[k]:20.1f}")
     return 0
 
 
@@ -142,10 +173,15 @@ def main(argv=None) -> int:
     t.add_argument("--copy-kernel", default="copy_calibration")
     t.add_argument("--workload", required=True)
     t.add_argument("--kernel-map", nargs="+", required=True)
+    t.add_argument("--calls", type=int, default=0,
+                   help="API calls in the profiled run (sum the matching dispatches over them)")
     t.add_argument("--json")
     t.add_argument("--source-hash")
+    c = sub.add_parser("counters")
+    c.add_argument("dir")
+    c.add_argument("--kernel", required=True, help="substring of the kernel name")
     args = ap.parse_args(argv)
-    return cmd_stats(args) if args.cmd == "stats" else cmd_traffic(args)
+    return {"stats": cmd_stats, "traffic": cmd_traffic, "counters": cmd_counters}[args.cmd](args)
 
 
 if __name__ == "__main__":

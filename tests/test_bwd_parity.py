@@ -47,7 +47,7 @@ def test_cls28_fwd_bwd_full(algo):
     check_grads(got, oracle_bwd(inp, wl.mask), torch.bfloat16, "cls28")
 
 
-SHAPES = [(1, 1), (1, 6), (6, 1), (2, 3), (5, 7), (7, 5), (16, 16), (28, 28), (9, 65), (65, 9),
+SHAPES = [(1, 1), (1, 6), (6, 1), (2, 3), (5, 7), (7, 5), (16, 16), (28, 28), (32, 32), (9, 65), (65, 9),
           (3, 130), (130, 3), (4, 300), (300, 4), (2, 1030), (1030, 2), (56, 56)]
 
 
@@ -62,6 +62,21 @@ def test_bwd_shapes(shape, dtype, algo):
     got = run_bwd(inp, 0xF, algo)
     torch.cuda.synchronize()
     check_grads(got, oracle_bwd(inp, 0xF), dtype, f"{H}x{W}")
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16], ids=["f32", "bf16"])
+@pytest.mark.parametrize("S", [16, 28, 32])
+@pytest.mark.parametrize("mask", [1, 2, 4, 8, 3, 12, 5, 15])
+def test_bwd_small_square_masks(mask, S, dtype):
+    """Small square planes (the LDS-staged kernel under AUTO): every direction
+    subset, an odd number of planes (a partial last group)."""
+    print(f"[bwd] square {S} mask {mask} {dtype}", flush=True)
+    t = synth.random_general((1, 3, S, S), ops.n_dirs(mask), device=DEV, seed=1000 + 16 * S + mask)
+    t = {k: v.to(dtype) for k, v in t.items()}
+    for algo in (L.GSPN_ALGO_AUTO, L.GSPN_ALGO_RESIDENT_GENERIC):
+        got = run_bwd(t, mask, algo)
+        torch.cuda.synchronize()
+        check_grads(got, oracle_bwd(t, mask), dtype, f"S={S} mask {mask} {ALGO_NAMES[algo]}")
 
 
 @pytest.mark.parametrize("algo", ALGOS, ids=lambda a: ALGO_NAMES[a])
