@@ -1,6 +1,7 @@
 // Resident-family kernels instantiated for bf16 storage (fp32 arithmetic).
 #include "gspn_resident_impl.hpp"
 #include "gspn_fixed_impl.hpp"
+#include "gspn_wide_impl.hpp"
 #include "gspn_staged_bwd_impl.hpp"
 
 namespace gspn {

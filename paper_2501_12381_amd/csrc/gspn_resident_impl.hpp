@@ -448,6 +448,7 @@ __global__ void __launch_bounds__(128, MINW) resident_fwd_kernel(ResFwdParams p)
 namespace gspn {
 inline bool fixed_size_supported(int H, int W);
 template <typename T, int S> hipError_t launch_fixed(const ResFwdParams& p, hipStream_t st);
+template <typename T> hipError_t launch_wide(const ResFwdParams& p, hipStream_t st);
 namespace resident_detail {
 
 constexpr int kMaxLds = 160 * 1024;  // LDS per CU on gfx950
@@ -531,6 +532,9 @@ hipError_t resident_fwd_t(const ResidentFwdArgs& a) {
   p.vec_y = (a.W % v16 == 0 && al(a.u, 16) && al(a.y, 16)) ? 2
           : (a.W % v8 == 0 && al(a.u, 8) && al(a.y, 8)) ? 1 : 0;
   hipStream_t st = (hipStream_t)a.stream;
+  if (a.use_fixed && a.H == 128 && a.W == 128 && al(a.x, 16) && al(a.lam, 16) && al(a.w, 16) && al(a.u, 16) &&
+      al(a.y, 16))
+    return launch_wide<T>(p, st);  // persistent, every input read once
   if (a.use_fixed && fixed_size_supported(a.H, a.W) && al(a.x, 16) && al(a.lam, 16) && al(a.w, 16)) {
     switch (a.H) {
       case 16: return launch_fixed<T, 16>(p, st);

@@ -138,6 +138,30 @@ def test_every_mask(mask, algo):
     assert_close(y, oracle_fwd(inp, mask), torch.float32, f"mask {mask}")
 
 
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16], ids=["f32", "bf16"])
+@pytest.mark.parametrize("mask", [1, 2, 4, 8, 3, 12, 5, 10, 7, 14, 15])
+def test_128_planes_every_direction_set(mask, dtype):
+    """128 x 128 planes (the persistent kernel that keeps lam*x on chip):
+    direction subsets, including phases with one or no present direction."""
+    print(f"[fwd] 128x128 mask {mask} {dtype}", flush=True)
+    inp = general_inputs(1, 3, 128, 128, mask, dtype, seed=100 + mask)
+    ref = oracle_fwd(inp, mask)
+    for algo in (L.GSPN_ALGO_AUTO, L.GSPN_ALGO_RESIDENT):
+        y = run_fwd(inp, mask, algo)
+        torch.cuda.synchronize()
+        assert_close(y, ref, dtype, f"mask {mask} algo {ALGO_NAMES[algo]}")
+
+
+@pytest.mark.parametrize("planes", [1, 255, 257, 600])
+def test_128_planes_per_workgroup_counts(planes):
+    """More and fewer planes than compute units: each workgroup walks its share."""
+    print(f"[fwd] 128x128 planes={planes}", flush=True)
+    inp = general_inputs(1, planes, 128, 128, 0xF, torch.bfloat16, seed=planes)
+    y = run_fwd(inp, 0xF, L.GSPN_ALGO_RESIDENT)
+    torch.cuda.synchronize()
+    assert_close(y, oracle_fwd(inp, 0xF), torch.bfloat16, f"planes {planes}")
+
+
 @pytest.mark.parametrize("algo", ALGOS, ids=lambda a: ALGO_NAMES[a])
 def test_single_direction_closed_form(algo):
     """Middle weight 1, others 0: each direction is a cumulative sum of lam*x."""
