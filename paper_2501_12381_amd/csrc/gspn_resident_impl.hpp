@@ -541,8 +541,7 @@ hipError_t resident_fwd_t(const ResidentFwdArgs& a) {
       case 28: return launch_fixed<T, 28>(p, st);
       case 32: return launch_fixed<T, 32>(p, st);
       case 56: return launch_fixed<T, 56>(p, st);
-      case 64: return launch_fixed<T, 64>(p, st);
-      default: return launch_fixed<T, 128>(p, st);
+      default: return launch_fixed<T, 64>(p, st);
     }
   }
   if (c.np == 1 && c.seg == 16) return launch_fwd_vl<T, 1, 16, true>(p, c, st);
