@@ -142,18 +142,15 @@ __device__ __forceinline__ void staged_forward(const T* __restrict__ w3, float* 
 }
 
 // One direction's adjoint from LDS; dw overwrites the consumed w entries and
-// g overwrites h.  Padding lanes (and lanes of absent planes) carry weights
-// forced to zero, so whatever g they hold never reaches a real lane; their
-// stores are skipped.  Their u * dy is finite (absent planes' is zero), which
-// keeps that g finite.
+// g overwrites h.  Padding lanes (and lanes of absent planes) hold g = 0, so
+// their finite weights (absent planes' are zero-filled) send nothing to a
+// real lane; their stores are skipped.
 template <typename T, int S, bool HZ, bool REV>
 __device__ __forceinline__ void staged_adjoint(const float* __restrict__ udy, T* __restrict__ w3,
                                                float* __restrict__ harr, int sl, bool lane_ok) {
   using C = StagedCfg<T, S>;
   constexpr int NP = S / 2;
   const bool valid = lane_ok && sl < S;
-  uint32_t vbits = valid ? 0xffffffffu : 0u;
-  asm volatile("" : "+v"(vbits));  // opaque: the w loads must not move under the store branch
   const int pos = valid ? sl : 0;
   const int aoff = valid ? (HZ ? sl * C::P : sl) : (HZ ? S * C::P : S);
   auto line_of = [](int s) { return REV ? s : S - 1 - s; };  // against the scan order
@@ -210,11 +207,10 @@ __device__ __forceinline__ void staged_adjoint(const float* __restrict__ udy, T*
       dv[t][1] = g * hpv;
       dv[t][2] = g * from_next_lane(hpv);
       gv[t] = g;
-      gn = g;
-      // padding lanes: weights forced to +0 whatever their bits
-      wn0 = __uint_as_float(__float_as_uint(cur[t][1]) & vbits);
-      wn1 = __uint_as_float(__float_as_uint(cur[t][2]) & vbits);
-      wn2 = __uint_as_float(__float_as_uint(cur[t][3]) & vbits);
+      gn = valid ? g : 0.f;
+      wn0 = cur[t][1];
+      wn1 = cur[t][2];
+      wn2 = cur[t][3];
       if constexpr (!HZ) {
         if (valid) {
           const int line = line_of(2 * j + t), e = elem(line);
@@ -270,6 +266,15 @@ __global__ void __launch_bounds__(256) staged_bwd_kernel(ResBwdParams p) {
     for (int i = tid; i < NA * NZ; i += 256) {
       const int a = i / NZ, k = i - a * NZ;
       s_arr[a * C::ARR + (k <= S ? k * C::P + S : S * C::P + (k - S - 1))] = 0.f;
+    }
+  }
+
+  // the weight maps of planes past the end of the tensor are zero-filled (the
+  // copies skip them; their lanes multiply these weights by g = 0)
+  if (np < PPW) {
+    for (int i = tid; i < 3 * ND * (PPW - np) * HW; i += 256) {
+      const int m = i / ((PPW - np) * HW), r = i - m * ((PPW - np) * HW);
+      s_flat[(SM_W + m) * C::MS + np * HW + r] = from_f<T>(0.f);
     }
   }
 
