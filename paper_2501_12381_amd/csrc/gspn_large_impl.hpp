@@ -320,7 +320,7 @@ __global__ void __launch_bounds__(64 * NW) large_h_kernel(LargeHParams p) {
   using C = LargeCfg<T>;
   constexpr int K = C::KH, HV = C::HV, VE = C::VE, KP = K + 1;
   typedef Pack<T, VE> PK;
-  extern __shared__ float lds[];  // [band_rows][KP] h of the band, then edges [2][NW][2]
+  extern __shared__ float lds[];  // [band_rows][KP] h of the band, edges [2][NW][2], 64 dummy slots
   float* edge = lds + p.band_rows * KP;
 
   // workgroup -> (direction, plane, band); consecutive ids (the bands of a plane,
@@ -370,17 +370,27 @@ __global__ void __launch_bounds__(64 * NW) large_h_kernel(LargeHParams p) {
   if (lane == 63) edge[(1 * NW + wave) * 2 + 1] = hp;
 
   float* hrow = lds + (in_band ? br : 0) * KP;
+  // edge slot of this lane per step parity: lanes 0 and 63 publish their row's
+  // h for the neighbouring waves, the other lanes write a private dummy slot
+  auto eslot = [&](int par) {
+    return lane == 0 ? (par * NW + wave) * 2 : (lane == 63 ? (par * NW + wave) * 2 + 1 : 4 * NW + lane);
+  };
+  const int eo0 = eslot(0), eo1 = eslot(1);
   auto scan = [&](auto rev_tag) __attribute__((always_inline)) {
     constexpr bool REV = decltype(rev_tag)::value;
-    // the tile is loaded in the order its columns are used, so the first
-    // columns are computed while the rest is still arriving
+    // the tile is loaded map by map, each row segment's vectors back to back:
+    // a lane's 128-byte line is then requested by consecutive instructions and
+    // is still in the L1 for all of them (vector-major order, which would let
+    // the first columns start earlier, re-fetches each line from L2 once per
+    // vector).  Scheduling barriers keep this issue order.
     PK tile[5][HV];
-    // (scheduling barriers keep this issue order)
 #pragma unroll
-    for (int i = 0; i < HV; ++i) {
-      const int v = REV ? HV - 1 - i : i;
+    for (int m = 0; m < 5; ++m) {
 #pragma unroll
-      for (int m = 0; m < 5; ++m) tile[m][v].load(base[m] + v * VE);
+      for (int i = 0; i < HV; ++i) {
+        const int v = REV ? HV - 1 - i : i;
+        tile[m][v].load(base[m] + v * VE);
+      }
       __builtin_amdgcn_sched_barrier(0);
     }
     lds_barrier();  // initial edges published
@@ -404,8 +414,7 @@ __global__ void __launch_bounds__(64 * NW) large_h_kernel(LargeHParams p) {
     h = fmaf(bw, hp, h);
     h = fmaf(cw, dn, h);
     hp = row_ok ? h : 0.f;
-    if (lane == 0) edge[(par * NW + wave) * 2 + 0] = hp;
-    if (lane == 63) edge[(par * NW + wave) * 2 + 1] = hp;
+    edge[par ? eo1 : eo0] = hp;  // one store for every lane (no branch per step)
     if (in_band) hrow[ti] = hp;
     lds_barrier();
   }
@@ -496,7 +505,7 @@ inline LargeGeom<T> large_geom(int H, int W) {
     g.nw = (g.band_rows + 2 * C::KH + 63) / 64;
   }
   g.nblk = (W + C::KH - 1) / C::KH;
-  g.lds_h = ((size_t)g.band_rows * (C::KH + 1) + 2 * 8 * 2) * sizeof(float);
+  g.lds_h = ((size_t)g.band_rows * (C::KH + 1) + 4 * 8 + 64) * sizeof(float);  // h, edges, dummy edge slots
   return g;
 }
 
