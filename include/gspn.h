@@ -94,9 +94,11 @@ enum {
   GSPN_ALGO_STREAM = 2,   /* one pass per direction through an fp32 workspace */
   GSPN_ALGO_RESIDENT_GENERIC = 3, /* resident family without size-specialised kernels */
   GSPN_ALGO_TWO_PASS = 4 /* forward only, for planes too large to keep on chip: the
-                            vertical pair of directions in one pass, the horizontal
-                            pair in blocks of 128-byte columns, partial sums in an
-                            fp32 workspace.  Needs W * element size a multiple of
+                            vertical directions in one pass, the horizontal pair in
+                            blocks of 128-byte columns, partial sums in an fp32
+                            workspace (two B*C*H*W arrays when both vertical
+                            directions and a horizontal one are in the mask, one
+                            otherwise).  Needs W * element size a multiple of
                             16 bytes and at least 128 bytes, W <= 4096 (bf16) or
                             2048 (f32), and 16-byte aligned x, w, lam, u, y. */
 };

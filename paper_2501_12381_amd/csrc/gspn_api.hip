@@ -121,16 +121,24 @@ bool resident_fits(const Problem& p, int dtype, bool backward) {
   return gspn::resident_fits((int)p.H, (int)p.W, dtype, backward);
 }
 
-// two-pass layout: fp32 partial sums (n > 1), then the column state of the
+// two-pass layout: fp32 partial sums (n > 1; a second array when both vertical
+// directions and a horizontal one are present: the vertical directions then
+// run as independent workgroups, one array each), then the column state of the
 // horizontal pass (2 parities x 2 directions x planes x H floats)
-size_t two_pass_acc_bytes(const Problem& p) { return p.n > 1 ? round_up((size_t)p.npc * 4, kWsAlign) : 0; }
+bool two_pass_split_v(uint32_t mask) {
+  return (mask & DIR_T2B) && (mask & DIR_B2T) && (mask & (DIR_L2R | DIR_R2L));
+}
+size_t two_pass_acc_bytes(const Problem& p, uint32_t mask) {
+  if (p.n <= 1) return 0;
+  return round_up((size_t)p.npc * 4, kWsAlign) * (two_pass_split_v(mask) ? 2 : 1);
+}
 size_t two_pass_state_bytes(const Problem& p, uint32_t mask) {
   return (mask & (DIR_L2R | DIR_R2L)) ? round_up((size_t)4 * p.planes * p.H * 4, kWsAlign) : 0;
 }
 
 size_t fwd_ws_bytes(const Problem& p, int algo, uint32_t mask) {
   if (algo == GSPN_ALGO_STREAM && p.n > 1) return round_up((size_t)p.npc * 4, kWsAlign);
-  if (algo == GSPN_ALGO_TWO_PASS) return two_pass_acc_bytes(p) + two_pass_state_bytes(p, mask);
+  if (algo == GSPN_ALGO_TWO_PASS) return two_pass_acc_bytes(p, mask) + two_pass_state_bytes(p, mask);
   return 0;
 }
 
@@ -198,7 +206,8 @@ int gspn_scan_fwd(const void* x, const void* w, const void* lam, const void* u, 
     LargeFwdArgs l{};
     l.x = x; l.lam = lam; l.w = w; l.u = u; l.y = y;
     l.acc = (float*)workspace;
-    l.state = (float*)((char*)workspace + two_pass_acc_bytes(p));
+    l.acc_b = two_pass_split_v(mask) ? (float*)((char*)workspace + round_up((size_t)p.npc * 4, kWsAlign)) : nullptr;
+    l.state = (float*)((char*)workspace + two_pass_acc_bytes(p, mask));
     l.mask = mask; l.planes = p.planes; l.H = (int)H; l.W = (int)W; l.dtype = dtype;
     l.stream = stream;
     return hip_status(large_fwd(l));

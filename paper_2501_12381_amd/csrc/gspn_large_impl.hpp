@@ -62,6 +62,9 @@ struct LargeVParams {
   int H, W;
   int slot0, slot1;  // weight slot of top-to-bottom / bottom-to-top, -1 when absent
   int final_out;     // nonzero: write y = u * sum; zero: write the fp32 partial sum
+  float* acc_b;      // split: the grid holds both directions as separate workgroups
+                     // (blockIdx / planes), bottom-to-top writing its h here
+  int split;
 };
 
 // Layout of a row over a wave: the wave's span of 64 * NP positions is cut into
@@ -85,9 +88,10 @@ __global__ void __launch_bounds__(128 * WPD, 2) large_v_kernel(LargeVParams p) {
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   constexpr bool both = BOTH, fin = FIN;
-  const int dir = both ? (wave >= WPD ? 1 : 0) : (p.slot0 >= 0 ? 0 : 1);
+  const int dir = both ? (wave >= WPD ? 1 : 0) : (p.split ? (blockIdx.x >= p.planes ? 1 : 0) : (p.slot0 >= 0 ? 0 : 1));
   const int wi = both ? wave - dir * WPD : wave;
-  const int64_t plane = blockIdx.x;
+  const int64_t plane = p.split && dir ? blockIdx.x - p.planes : blockIdx.x;
+  float* const accw = p.split && dir ? p.acc_b : p.acc;  // where a single direction's h goes
   const int H = p.H, W = p.W;
   // per chunk: position of the lane's first element, whether it is in the row
   int po[NQ];
@@ -236,7 +240,7 @@ __global__ void __launch_bounds__(128 * WPD, 2) large_v_kernel(LargeVParams p) {
             stv<G>(p.acc + pb + off + po[q], o);
           }
         } else {
-          stv<G>(p.acc + pb + off + po[q], hp[q]);
+          stv<G>(accw + pb + off + po[q], hp[q]);
         }
       }
     }
@@ -313,6 +317,7 @@ struct LargeHParams {
   int half;           // first launch of the second half (pairs)
   int band_rows, nbands, halo;
   int has_v;          // acc holds the vertical pass's partial sum
+  const float* acc_b; // non-null: the vertical sum is acc + acc_b until the first horizontal direction adds
 };
 
 template <typename T, int NW>
@@ -430,6 +435,7 @@ __global__ void __launch_bounds__(64 * NW) large_h_kernel(LargeHParams p) {
   const bool second = both && p.step >= p.half;
   const bool fin = !both || second;
   const bool read_acc = second || p.has_v;
+  const bool add_b = p.acc_b != nullptr && !second;  // the vertical sum still lives in two arrays
   const int rows = min(p.band_rows, H - band * p.band_rows);
   const int nvr = (K - lo) / VE;
   const int n = rows * nvr;
@@ -437,7 +443,7 @@ __global__ void __launch_bounds__(64 * NW) large_h_kernel(LargeHParams p) {
   constexpr int U = (C::HROWS * (K / VE) + 64 * NW - 1) / (64 * NW) < 8
                         ? (C::HROWS * (K / VE) + 64 * NW - 1) / (64 * NW) : 8;
   for (int e0 = tid; e0 < n; e0 += 64 * NW * U) {
-    float av[U][VE];
+    float av[U][VE], bv[U][VE];
     Pack<T, VE> uv[U];
 #pragma unroll
     for (int k = 0; k < U; ++k) {
@@ -445,6 +451,7 @@ __global__ void __launch_bounds__(64 * NW) large_h_kernel(LargeHParams p) {
       const int rr = e / nvr, cc = lo + (e - rr * nvr) * VE;
       const int64_t o = ob + (int64_t)rr * W + cc;
       if (read_acc) ldv<VE>(p.acc + o, av[k]);
+      if (add_b) ldv<VE>(p.acc_b + o, bv[k]);
       if (fin) uv[k].load((const T*)p.u + o);
     }
 #pragma unroll
@@ -455,7 +462,8 @@ __global__ void __launch_bounds__(64 * NW) large_h_kernel(LargeHParams p) {
         const int64_t o = ob + (int64_t)rr * W + cc;
         float s[VE];
 #pragma unroll
-        for (int q = 0; q < VE; ++q) s[q] = (read_acc ? av[k][q] : 0.f) + lds[rr * KP + cc + q];
+        for (int q = 0; q < VE; ++q)
+          s[q] = (read_acc ? (add_b ? av[k][q] + bv[k][q] : av[k][q]) : 0.f) + lds[rr * KP + cc + q];
         if (fin) {
 #pragma unroll
           for (int q = 0; q < VE; ++q) s[q] *= uv[k].get(q);
@@ -511,7 +519,7 @@ inline LargeGeom<T> large_geom(int H, int W) {
 
 template <typename T, int WPD, bool BOTH, bool FIN>
 hipError_t launch_large_v_mode(const LargeVParams& p, hipStream_t st) {
-  hipLaunchKernelGGL((large_v_kernel<T, WPD, BOTH, FIN>), dim3((unsigned)p.planes),
+  hipLaunchKernelGGL((large_v_kernel<T, WPD, BOTH, FIN>), dim3((unsigned)(p.planes * (p.split ? 2 : 1))),
                      dim3((BOTH ? 128 : 64) * WPD), 0, st, p);
   return hipGetLastError();
 }
@@ -567,7 +575,13 @@ hipError_t large_fwd_t(const LargeFwdArgs& a) {
     v.planes = a.planes; v.npc = npc; v.H = a.H; v.W = a.W;
     v.slot0 = slot[0]; v.slot1 = slot[1];
     v.final_out = has_h ? 0 : 1;
-    const bool both = slot[0] >= 0 && slot[1] >= 0;
+    // both vertical directions feeding a horizontal pass: twice the workgroups,
+    // one direction each, each with its own partial sum (no midpoint pairing,
+    // so the grid has no partly filled last round of whole planes)
+    v.split = slot[0] >= 0 && slot[1] >= 0 && has_h && a.acc_b != nullptr;
+    v.acc_b = a.acc_b;
+    if (v.split && 2 * a.planes > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+    const bool both = slot[0] >= 0 && slot[1] >= 0 && !v.split;
     hipError_t e;
     switch (g.wpd) {
       case 1: e = launch_large_v<T, 1>(v, both, st); break;
@@ -588,6 +602,7 @@ hipError_t large_fwd_t(const LargeFwdArgs& a) {
   h.half = both ? g.nblk / 2 + h.delay : 0;
   h.band_rows = g.band_rows; h.nbands = g.nbands; h.halo = g.halo;
   h.has_v = has_v ? 1 : 0;
+  h.acc_b = (slot[0] >= 0 && slot[1] >= 0 && a.acc_b != nullptr) ? a.acc_b : nullptr;
   const int64_t grid = (int64_t)g.nbands * a.planes * (both ? 2 : 1);
   if (grid > 0x7fffffffLL) return hipErrorInvalidConfiguration;
   for (int j = 0; j < g.nblk + h.delay; ++j) {

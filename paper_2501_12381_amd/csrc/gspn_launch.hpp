@@ -120,6 +120,8 @@ struct LargeFwdArgs {
   const void* u;
   void* y;
   float* acc;      // fp32 partial sums, B*C*H*W (needed when n > 1)
+  float* acc_b;    // second partial-sum array: bottom-to-top's h when both vertical
+                   // directions and a horizontal one are present (else null)
   float* state;    // 2 * 2 * B*C*H floats (needed with a horizontal direction)
   uint32_t mask;
   int64_t planes;

@@ -69,21 +69,24 @@ def test_workspace_sizes():
     assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 7, 0xF, bf, S) % 256 == 0
     # streaming backward: previous-line state, sum of h, sum of g (fp32 each)
     assert L.gspn_scan_bwd_workspace_bytes(2, 3, 5, 7, 0xF, f32, S) >= 3 * npc * 4
-    # two-pass forward: fp32 partial sums (several directions), then the column
-    # state of the horizontal pass (2 parities x 2 directions x planes x H floats)
+    # two-pass forward: fp32 partial sums (several directions; two arrays when
+    # both vertical directions feed a horizontal pass), then the column state of
+    # the horizontal pass (2 parities x 2 directions x planes x H floats)
     T = L.GSPN_ALGO_TWO_PASS
     acc, state = 2 * 3 * 5 * 64 * 4, 512  # 7680 is a multiple of 256; 4*6*5*4 = 480 -> 512
-    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 64, 0xF, bf, T) == acc + state
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 64, 0xF, bf, T) == 2 * acc + state
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 64, 0x7, bf, T) == 2 * acc + state
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 64, 0xD, bf, T) == acc + state
     assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 64, 0x3, bf, T) == acc
     assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 64, 0x4, bf, T) == state
     assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 64, 0x1, bf, T) == 0
     assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 60, 0xF, bf, T) == 0  # W*2 not a multiple of 16
     assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 56, 0xF, bf, T) == 0  # row under 128 bytes
-    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 32, 0xF, f32, T) == 2 * 3 * 5 * 32 * 4 + 512
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 32, 0xF, f32, T) == 2 * (2 * 3 * 5 * 32 * 4) + 512
     assert L.gspn_scan_bwd_workspace_bytes(2, 3, 5, 64, 0xF, bf, T) == 0  # forward only
     # AUTO takes the two-pass kernels for planes that do not fit on chip
     big = L.gspn_scan_fwd_workspace_bytes(1, 2, 2048, 2048, 0xF, bf, L.GSPN_ALGO_AUTO)
-    assert big == 2 * 2048 * 2048 * 4 + 4 * 2 * 2048 * 4
+    assert big == 2 * (2 * 2048 * 2048 * 4) + 4 * 2 * 2048 * 4
     # invalid problems report 0
     assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 7, 0, f32, S) == 0
     assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 7, 1, 7, S) == 0
