@@ -14,10 +14,11 @@
 //            takes lam * x of the other half, and the accumulator, from LDS.
 //   phase H  wave 0 scans left-to-right, wave 1 right-to-left, each lane
 //            owning two adjacent rows.  Weights arrive as 128-byte row
-//            segments (whole cache lines, one per lane and load), refilled one
-//            16-byte vector at a time as soon as its columns are consumed;
+//            segments (whole cache lines) into two register tiles, the next
+//            tile's segments staggered over the current tile's columns;
 //            lam * x and the accumulator come from LDS.
-//   epilogue y = u * acc, whole rows per load and store.
+//   epilogue y = u * acc, whole rows per store; u is requested during the
+//            last horizontal tile.
 //
 // The order of the additions is the one of the resident kernels: in each
 // phase the first half's direction adds before the second half's, and the
@@ -219,45 +220,53 @@ __device__ __forceinline__ void wide_v(const wide_rsrc_t (&rb)[5], float* __rest
 }
 
 // Phase H for one wave (the direction is present).  rw: plane resources of
-// w0..w2.  One loop iteration per tile; vector v of the register tile always
-// holds columns [v VE, v VE + VE) of the current tile, and is refilled with the
-// next tile's as soon as its last column is used, which keeps a steady stream
-// of loads in flight under the arithmetic (past the last tile the refill
-// reads nothing).
+// w0..w2.  Two register tiles: tile t is consumed from one while tile t + 1
+// arrives in the other, requested as whole 128-byte row segments (a line's
+// eight 16-byte pieces in consecutive instructions, so it is fetched into the
+// L1 once) and staggered over tile t's columns, which keeps a steady stream
+// of loads under the arithmetic.  During the last tile the wave requests its
+// epilogue rows of u instead (ru; into ur).
 template <typename T, bool REV>
 __device__ __forceinline__ void wide_h(const wide_rsrc_t (&rw)[3], float* __restrict__ acc,
-                                       const float* __restrict__ lxa, int lane) {
+                                       const float* __restrict__ lxa, int lane, int wave, wide_rsrc_t ru,
+                                       Pack<T, WideCfg<T>::NP> (&ur)[WideCfg<T>::S / 2]) {
   using C = WideCfg<T>;
   constexpr int S = C::S, NP = C::NP, P = C::P, G = C::G;
   constexpr int VE = C::VE, TH = C::TH, NV = C::NV, NTH = C::NTH;
-  static_assert(TH % G == 0, "lookahead slots repeat with the tile");
+  constexpr int NL = 3 * NP, GAP = TH / NL;  // row segments per tile, steps between their requests
+  constexpr int UPS = (S / 2 + TH - 1) / TH;  // u rows requested per step of the last tile
+  static_assert(TH % G == 0 && GAP >= 1, "lookahead slots repeat with the tile");
   typedef Pack<T, VE> PK;
   const int row0 = lane * NP;
-  auto tile_so = [](int t) { return t < NTH ? (REV ? NTH - 1 - t : t) * TH * (int)sizeof(T) : kWideOob; };
+  auto tile_so = [](int t) { return (REV ? NTH - 1 - t : t) * TH * (int)sizeof(T); };
 
-  PK tile[3][NP][NV];
+  PK tile[2][3][NP][NV];
   int voff[NP];
 #pragma unroll
   for (int q = 0; q < NP; ++q) voff[q] = (row0 + q) * S * (int)sizeof(T);
-  auto load_vec = [&](int v, int so) __attribute__((always_inline)) {
+  auto load_seg = [&](PK (&tb)[3][NP][NV], int m, int q, int so) __attribute__((always_inline)) {
 #pragma unroll
-    for (int m = 0; m < 3; ++m)
-#pragma unroll
-      for (int q = 0; q < NP; ++q) wide_load(tile[m][q][v], rw[m], voff[q], so + v * VE * (int)sizeof(T));
+    for (int i = 0; i < NV; ++i) {
+      const int v = REV ? NV - 1 - i : i;  // the order the columns are used
+      wide_load(tb[m][q][v], rw[m], voff[q], so + v * VE * (int)sizeof(T));
+    }
   };
-  // first tile, vectors in the order they are consumed
 #pragma unroll
-  for (int i = 0; i < NV; ++i) load_vec(REV ? NV - 1 - i : i, tile_so(0));
+  for (int m = 0; m < 3; ++m)
+#pragma unroll
+    for (int q = 0; q < NP; ++q) load_seg(tile[0], m, q, tile_so(0));
 
+  const int uvoff = lane * NP * (int)sizeof(T);
   float hp[NP];
 #pragma unroll
   for (int q = 0; q < NP; ++q) hp[q] = 0.f;
   float la[G][NP], aa[G][NP];
 
+#pragma unroll
   for (int t = 0; t < NTH; ++t) {
+    const int b = t & 1;
     if (t == NTH / 2) lds_barrier();  // middle: the other wave's first-half additions are done
     const int c0 = (REV ? NTH - 1 - t : t) * TH;
-    const int so_next = tile_so(t + 1);
     auto lds_read = [&](float (&l)[NP], float (&a)[NP], int e) __attribute__((always_inline)) {
 #pragma unroll
       for (int q = 0; q < NP; ++q) {
@@ -272,19 +281,26 @@ __device__ __forceinline__ void wide_h(const wide_rsrc_t (&rw)[3], float* __rest
     for (int i = 0; i < TH; ++i) {
       const int e = REV ? TH - 1 - i : i;  // column inside the tile
       const int v = e / VE, el = e % VE, gi = i % G;
-      float lx[NP], av[NP], a[NP], b[NP], c[NP];
+      float lx[NP], av[NP], a[NP], bb[NP], c[NP];
 #pragma unroll
       for (int q = 0; q < NP; ++q) {
         lx[q] = la[gi][q];
         av[q] = aa[gi][q];
-        a[q] = tile[0][q][v].get(el);
-        b[q] = tile[1][q][v].get(el);
-        c[q] = tile[2][q][v].get(el);
+        a[q] = tile[b][0][q][v].get(el);
+        bb[q] = tile[b][1][q][v].get(el);
+        c[q] = tile[b][2][q][v].get(el);
       }
-      // the vector's last column in scan order: refill it with the next tile's
-      if (REV ? el == 0 : el == VE - 1) load_vec(v, so_next);
+      if (t + 1 < NTH) {
+        if (i % GAP == 0 && i / GAP < NL) load_seg(tile[1 - b], (i / GAP) / NP, (i / GAP) % NP, tile_so(t + 1));
+      } else {
+#pragma unroll
+        for (int k = 0; k < UPS; ++k) {
+          const int r = i * UPS + k;
+          if (r < S / 2) wide_load(ur[r], ru, uvoff, (wave * (S / 2) + r) * S * (int)sizeof(T));
+        }
+      }
       if (i + G < TH) lds_read(la[gi], aa[gi], REV ? TH - 1 - (i + G) : i + G);
-      wide_step<NP>(lx, a, b, c, hp);
+      wide_step<NP>(lx, a, bb, c, hp);
 #pragma unroll
       for (int q = 0; q < NP; ++q) acc[(row0 + q) * P + c0 + e] = av[q] + hp[q];
     }
@@ -292,25 +308,21 @@ __device__ __forceinline__ void wide_h(const wide_rsrc_t (&rw)[3], float* __rest
 }
 
 // y = u * acc: wave w writes rows [64 w, 64 w + 64), each lane two adjacent
-// columns of a row (whole-row loads and stores, LDS reads without conflicts
-// beyond two-way), B rows in flight.
+// columns of a row (whole-row stores, LDS reads without conflicts beyond
+// two-way); u of those rows is already in registers (ur).
 template <typename T>
-__device__ __forceinline__ void wide_epilogue(wide_rsrc_t ru, wide_rsrc_t ry, const float* __restrict__ acc,
-                                              int lane, int wave) {
+__device__ __forceinline__ void wide_epilogue(const Pack<T, WideCfg<T>::NP> (&ur)[WideCfg<T>::S / 2], wide_rsrc_t ry,
+                                              const float* __restrict__ acc, int lane, int wave) {
   using C = WideCfg<T>;
-  constexpr int S = C::S, NP = C::NP, P = C::P, B = 16;
+  constexpr int S = C::S, NP = C::NP, P = C::P;
   const int col = lane * NP, voff = col * (int)sizeof(T);
-  for (int r0 = wave * (S / 2); r0 < (wave + 1) * (S / 2); r0 += B) {
-    Pack<T, NP> u[B];
 #pragma unroll
-    for (int b = 0; b < B; ++b) wide_load(u[b], ru, voff, (r0 + b) * S * (int)sizeof(T));
+  for (int r = 0; r < S / 2; ++r) {
+    const int row = wave * (S / 2) + r;
+    float y[NP];
 #pragma unroll
-    for (int b = 0; b < B; ++b) {
-      float y[NP];
-#pragma unroll
-      for (int q = 0; q < NP; ++q) y[q] = u[b].get(q) * acc[(r0 + b) * P + col + q];
-      wide_store<T, NP>(y, ry, voff, (r0 + b) * S * (int)sizeof(T));
-    }
+    for (int q = 0; q < NP; ++q) y[q] = ur[r].get(q) * acc[row * P + col + q];
+    wide_store<T, NP>(y, ry, voff, row * S * (int)sizeof(T));
   }
 }
 
@@ -345,20 +357,26 @@ __global__ void __launch_bounds__(128, 1) wide_fwd_kernel(ResFwdParams p) {
       }
     }
     __syncthreads();
-    // phase H: wave 0 left-to-right, wave 1 right-to-left
+    // phase H: wave 0 left-to-right, wave 1 right-to-left; each wave's rows of
+    // u for the epilogue arrive during its last tile
+    const wide_rsrc_t ru = wide_rsrc((const T*)p.u + pof, PB);
+    Pack<T, C::NP> ur[S / 2];
     {
       const int slot = p.slot[2 + wave];
       if (slot < 0) {
+        const int uvoff = lane * C::NP * (int)sizeof(T);
+#pragma unroll
+        for (int r = 0; r < S / 2; ++r) wide_load(ur[r], ru, uvoff, (wave * (S / 2) + r) * S * (int)sizeof(T));
         lds_barrier();  // the middle barrier of the phase
       } else {
         const T* w0 = (const T*)p.w + (int64_t)slot * 3 * p.npc + pof;
         const wide_rsrc_t rw[3] = {wide_rsrc(w0, PB), wide_rsrc(w0 + p.npc, PB), wide_rsrc(w0 + 2 * p.npc, PB)};
-        if (wave == 0) wide_h<T, false>(rw, acc, lxa, lane);
-        else wide_h<T, true>(rw, acc, lxa, lane);
+        if (wave == 0) wide_h<T, false>(rw, acc, lxa, lane, wave, ru, ur);
+        else wide_h<T, true>(rw, acc, lxa, lane, wave, ru, ur);
       }
     }
     __syncthreads();
-    wide_epilogue<T>(wide_rsrc((const T*)p.u + pof, PB), wide_rsrc((T*)p.y + pof, PB), acc, lane, wave);
+    wide_epilogue<T>(ur, wide_rsrc((T*)p.y + pof, PB), acc, lane, wave);
     __syncthreads();  // the next plane overwrites both arrays
   }
 }
