@@ -35,6 +35,16 @@
 
 namespace gspn {
 
+// Calls f(std::integral_constant<int, i>) for i = B .. E-1 (compile-time indices,
+// fully unrolled by construction).
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
+
 template <typename T>
 struct LargeCfg {
   static constexpr int VE = 16 / (int)sizeof(T);   // elements per 16-byte vector
@@ -381,6 +391,32 @@ __global__ void __launch_bounds__(64 * NW) large_h_kernel(LargeHParams p) {
     return lane == 0 ? (par * NW + wave) * 2 : (lane == 63 ? (par * NW + wave) * 2 + 1 : 4 * NW + lane);
   };
   const int eo0 = eslot(0), eo1 = eslot(1);
+  // epilogue operands: the first UP vectors of each thread are requested
+  // during the last quarter of the scan (their tile registers are dead by
+  // then), so the epilogue finds them in registers
+  const bool second = both && p.step >= p.half;
+  const bool fin = !both || second;
+  const bool read_acc = second || p.has_v;
+  const bool add_b = p.acc_b != nullptr && !second;  // the vertical sum still lives in two arrays
+  const int rows = min(p.band_rows, H - band * p.band_rows);
+  const int nvr = (K - lo) / VE;
+  const int n = rows * nvr;
+  const int64_t ob = plane * HW + (int64_t)band * p.band_rows * W + ws;
+  constexpr int TT = 64 * NW, UP = 6, PF = K - K / 4;
+  float pav[UP][VE], pbv[UP][VE];
+  Pack<T, VE> puv[UP];
+  auto prefetch = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int k = 0; k < UP; ++k) {
+      const int e = tid + k * TT < n ? tid + k * TT : 0;
+      const int rr = e / nvr, cc = lo + (e - rr * nvr) * VE;
+      const int64_t o = ob + (int64_t)rr * W + cc;
+      if (read_acc) ldv<VE>(p.acc + o, pav[k]);
+      if (add_b) ldv<VE>(p.acc_b + o, pbv[k]);
+      if (fin) puv[k].load((const T*)p.u + o);
+    }
+  };
+
   auto scan = [&](auto rev_tag) __attribute__((always_inline)) {
     constexpr bool REV = decltype(rev_tag)::value;
     // the tile is loaded map by map, each row segment's vectors back to back:
@@ -399,30 +435,34 @@ __global__ void __launch_bounds__(64 * NW) large_h_kernel(LargeHParams p) {
       __builtin_amdgcn_sched_barrier(0);
     }
     lds_barrier();  // initial edges published
-#pragma unroll
-  for (int i = 0; i < K; ++i) {
-    const int ti = REV ? K - 1 - i : i;  // window column of this step
-    if (ti < lo) continue;               // short last block (uniform)
-    const int par = i & 1;
-    float up = from_prev_lane(hp), dn = from_next_lane(hp);
-    if constexpr (NW > 1) {
-      const float nu = edge[((par ^ 1) * NW + (wave > 0 ? wave - 1 : wave)) * 2 + 1];
-      const float nd = edge[((par ^ 1) * NW + (wave < NW - 1 ? wave + 1 : wave)) * 2 + 0];
-      if (lane == 0) up = wave > 0 ? nu : 0.f;
-      if (lane == 63) dn = wave < NW - 1 ? nd : 0.f;
-    }
-    const float xv = tile[0][ti / VE].get(ti % VE), lv = tile[1][ti / VE].get(ti % VE);
-    const float a = tile[2][ti / VE].get(ti % VE), bw = tile[3][ti / VE].get(ti % VE),
-                cw = tile[4][ti / VE].get(ti % VE);
-    float h = lv * xv;
-    h = fmaf(a, up, h);
-    h = fmaf(bw, hp, h);
-    h = fmaf(cw, dn, h);
-    hp = row_ok ? h : 0.f;
-    edge[par ? eo1 : eo0] = hp;  // one store for every lane (no branch per step)
-    if (in_band) hrow[ti] = hp;
-    lds_barrier();
-  }
+    auto step = [&](auto ic) __attribute__((always_inline)) {
+      constexpr int i = decltype(ic)::value;
+      const int ti = REV ? K - 1 - i : i;  // window column of this step
+      if (ti < lo) return;                 // short last block (uniform)
+      const int par = i & 1;
+      float up = from_prev_lane(hp), dn = from_next_lane(hp);
+      if constexpr (NW > 1) {
+        const float nu = edge[((par ^ 1) * NW + (wave > 0 ? wave - 1 : wave)) * 2 + 1];
+        const float nd = edge[((par ^ 1) * NW + (wave < NW - 1 ? wave + 1 : wave)) * 2 + 0];
+        if (lane == 0) up = wave > 0 ? nu : 0.f;
+        if (lane == 63) dn = wave < NW - 1 ? nd : 0.f;
+      }
+      const float xv = tile[0][ti / VE].get(ti % VE), lv = tile[1][ti / VE].get(ti % VE);
+      const float a = tile[2][ti / VE].get(ti % VE), bw = tile[3][ti / VE].get(ti % VE),
+                  cw = tile[4][ti / VE].get(ti % VE);
+      float h = lv * xv;
+      h = fmaf(a, up, h);
+      h = fmaf(bw, hp, h);
+      h = fmaf(cw, dn, h);
+      hp = row_ok ? h : 0.f;
+      edge[par ? eo1 : eo0] = hp;  // one store for every lane (no branch per step)
+      if (in_band) hrow[ti] = hp;
+      lds_barrier();
+    };
+    // two unrolled runs of steps, the epilogue's loads requested between them
+    static_for<0, PF + 1>([&](auto ic) __attribute__((always_inline)) { step(ic); });
+    prefetch();
+    static_for<PF + 1, K>([&](auto ic) __attribute__((always_inline)) { step(ic); });
   };
   if (dir) scan(std::true_type{});
   else scan(std::false_type{});
@@ -430,24 +470,32 @@ __global__ void __launch_bounds__(64 * NW) large_h_kernel(LargeHParams p) {
   __syncthreads();
 
   // combine the band's h with acc: y = u * (acc + h) or acc + h, one 16-byte
-  // vector of T (VE columns) a thread; all loads of a thread are issued before
-  // any is used, so the epilogue waits for memory once
-  const bool second = both && p.step >= p.half;
-  const bool fin = !both || second;
-  const bool read_acc = second || p.has_v;
-  const bool add_b = p.acc_b != nullptr && !second;  // the vertical sum still lives in two arrays
-  const int rows = min(p.band_rows, H - band * p.band_rows);
-  const int nvr = (K - lo) / VE;
-  const int n = rows * nvr;
-  const int64_t ob = plane * HW + (int64_t)band * p.band_rows * W + ws;
-  constexpr int U = (C::HROWS * (K / VE) + 64 * NW - 1) / (64 * NW) < 8
-                        ? (C::HROWS * (K / VE) + 64 * NW - 1) / (64 * NW) : 8;
-  for (int e0 = tid; e0 < n; e0 += 64 * NW * U) {
+  // vector of T (VE columns) a thread: first the prefetched vectors, then any
+  // beyond them in batches whose loads are all issued before any is used
+  auto combine = [&](int e, const float* av, const float* bv, const Pack<T, VE>& uv) __attribute__((always_inline)) {
+    const int rr = e / nvr, cc = lo + (e - rr * nvr) * VE;
+    const int64_t o = ob + (int64_t)rr * W + cc;
+    float s[VE];
+#pragma unroll
+    for (int q = 0; q < VE; ++q) s[q] = (read_acc ? (add_b ? av[q] + bv[q] : av[q]) : 0.f) + lds[rr * KP + cc + q];
+    if (fin) {
+#pragma unroll
+      for (int q = 0; q < VE; ++q) s[q] *= uv.get(q);
+      stv<VE>((T*)p.y + o, s);
+    } else {
+      stv<VE>(p.acc + o, s);
+    }
+  };
+#pragma unroll
+  for (int k = 0; k < UP; ++k)
+    if (tid + k * TT < n) combine(tid + k * TT, pav[k], pbv[k], puv[k]);
+  constexpr int U = 8;
+  for (int e0 = tid + UP * TT; e0 < n; e0 += TT * U) {
     float av[U][VE], bv[U][VE];
     Pack<T, VE> uv[U];
 #pragma unroll
     for (int k = 0; k < U; ++k) {
-      const int e = e0 + k * 64 * NW < n ? e0 + k * 64 * NW : e0;
+      const int e = e0 + k * TT < n ? e0 + k * TT : e0;
       const int rr = e / nvr, cc = lo + (e - rr * nvr) * VE;
       const int64_t o = ob + (int64_t)rr * W + cc;
       if (read_acc) ldv<VE>(p.acc + o, av[k]);
@@ -455,24 +503,8 @@ __global__ void __launch_bounds__(64 * NW) large_h_kernel(LargeHParams p) {
       if (fin) uv[k].load((const T*)p.u + o);
     }
 #pragma unroll
-    for (int k = 0; k < U; ++k) {
-      const int e = e0 + k * 64 * NW;
-      if (e < n) {
-        const int rr = e / nvr, cc = lo + (e - rr * nvr) * VE;
-        const int64_t o = ob + (int64_t)rr * W + cc;
-        float s[VE];
-#pragma unroll
-        for (int q = 0; q < VE; ++q)
-          s[q] = (read_acc ? (add_b ? av[k][q] + bv[k][q] : av[k][q]) : 0.f) + lds[rr * KP + cc + q];
-        if (fin) {
-#pragma unroll
-          for (int q = 0; q < VE; ++q) s[q] *= uv[k].get(q);
-          stv<VE>((T*)p.y + o, s);
-        } else {
-          stv<VE>(p.acc + o, s);
-        }
-      }
-    }
+    for (int k = 0; k < U; ++k)
+      if (e0 + k * TT < n) combine(e0 + k * TT, av[k], bv[k], uv[k]);
   }
 }
 
