@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace gspn {
 
 typedef __bf16 bf16;
@@ -112,6 +114,16 @@ __device__ __forceinline__ float from_next_lane(float v) {
 // useful across the barriers of a scan.
 __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// Calls f(std::integral_constant<int, i>) for i = B .. E-1 (compile-time indices,
+// fully unrolled by construction, where a large unrolled loop body may not be).
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
 }
 
 }  // namespace gspn

@@ -27,23 +27,11 @@
 // are reproducible run to run.
 #pragma once
 
-#include <type_traits>
-
 #include "gspn_device.hpp"
 #include "gspn_launch.hpp"
 #include "gspn_resident_impl.hpp"
 
 namespace gspn {
-
-// Calls f(std::integral_constant<int, i>) for i = B .. E-1 (compile-time indices,
-// fully unrolled by construction).
-template <int B, int E, typename F>
-__device__ __forceinline__ void static_for(F&& f) {
-  if constexpr (B < E) {
-    f(std::integral_constant<int, B>{});
-    static_for<B + 1, E>(f);
-  }
-}
 
 template <typename T>
 struct LargeCfg {

@@ -1,29 +1,27 @@
 // Persistent forward kernel for 128 x 128 planes.
 //
-// One workgroup of two waves per compute unit walks its share of the planes
+// One workgroup of four waves per compute unit walks its share of the planes
 // one plane at a time, so a batch of planes costs ceil(planes / CUs) plane
 // times with no partly filled last round.  LDS holds two fp32 arrays of the
 // plane (row pitch 129): the accumulator of sum_d h_d, and lam * x.  Every
-// input element is read from HBM exactly once:
+// input element is read from HBM exactly once.  Waves 0 and 1 scan the
+// vertical directions (top-to-bottom, bottom-to-top; a lane owns two adjacent
+// columns), waves 2 and 3 the horizontal ones (left-to-right, right-to-left;
+// a lane owns two adjacent rows), so the two kinds of scan overlap:
 //
-//   phase V  wave 0 scans top-to-bottom, wave 1 bottom-to-top, each lane
-//            owning two adjacent columns.  In the first half of the phase a
-//            wave reads x, lam and its three weights for the rows it reaches
-//            first, stores lam * x and its h (a plain store: nothing was there
-//            before); after the middle barrier it reads only its weights and
-//            takes lam * x of the other half, and the accumulator, from LDS.
-//   phase H  wave 0 scans left-to-right, wave 1 right-to-left, each lane
-//            owning two adjacent rows.  Weights arrive as 128-byte row
-//            segments (whole cache lines) into two register tiles, the next
-//            tile's segments staggered over the current tile's columns;
-//            lam * x and the accumulator come from LDS.
-//   epilogue y = u * acc, whole rows per store; u is requested during the
-//            last horizontal tile.
+//   B0..B1   the vertical waves store lam * x and h of the rows each reached
+//            first (computed in registers during the previous plane's tail)
+//   B1..B2   vertical second halves (lam * x from LDS, h kept in registers)
+//            alongside the horizontal first halves (adding h to acc)
+//   B2..B3   the vertical waves add their second-half h to acc
+//   B3..     horizontal second halves, then y = u * acc by the horizontal
+//            waves (each for the columns its second half covers), alongside
+//            the vertical first halves of the next plane
 //
-// The order of the additions is the one of the resident kernels: in each
-// phase the first half's direction adds before the second half's, and the
-// vertical pair before the horizontal pair.  A direction absent from the mask
-// costs nothing but its barriers (in phase V its wave still stores lam * x
+// Every element of acc receives its terms in a fixed order (first vertical
+// half, first horizontal half, second vertical half, second horizontal half),
+// so results are reproducible run to run.  A direction absent from the mask
+// costs nothing but its barriers (its vertical wave still supplies lam * x
 // and zeros for its first-half rows).
 #pragma once
 
@@ -48,8 +46,9 @@ struct WideCfg {
   static constexpr int NV = TH / VE;             // 16-byte vectors per row segment
   static constexpr int NTH = S / TH;             // tiles per horizontal phase
   static constexpr int G = 4;                    // LDS lookahead (steps)
+  static constexpr int NT = 256;                 // two vertical and two horizontal waves
   static constexpr int LDS_BYTES = 2 * ARR * 4;
-  static_assert(MID % RV == 0 && MID % TH == 0, "ring and tiles must align with the middle line");
+  static_assert(MID % RV == 0 && MID % TH == 0 && NTH % 2 == 0, "ring and tiles must align with the middle line");
 };
 
 // Buffer loads: the plane base and size live in a scalar resource, the lane
@@ -113,48 +112,65 @@ __device__ __forceinline__ void wide_step(const float (&lx)[NP], const float (&a
 // without a branch around the loads.
 constexpr int kWideOob = 0x40000000;
 
-// Phase V for one wave.  PRESENT: the direction is in the mask.  rb: plane
-// resources of x, lam, w0, w1, w2.  The steps run as a loop over ring turns
-// (R rows per iteration): straight-line code for all rows would not fit the
-// instruction cache.
+// Vertical role (waves 0 and 1): the wave's direction for every plane of the
+// workgroup.  Per plane, in the wave's row order s = 0 .. S-1:
+//   first half  (s < MID): x, lam and the weights from HBM; lam * x and h are
+//               kept in registers (lxr, hr) and stored to LDS only at the next
+//               plane's start, since this half runs while the horizontal
+//               waves still use the previous plane's arrays;
+//   second half (s >= MID): the weights from HBM, lam * x from LDS (stored by
+//               the other vertical wave); h is kept in registers (hv) and added
+//               to acc once the horizontal first halves are done with it.
+// A ring of R rows keeps the loads in flight across steps, barriers and
+// planes: the last steps of a plane request the next plane's first rows.
+// PRESENT: the direction is in the mask (otherwise the wave only supplies
+// lam * x and zeros for its first-half rows).
 template <typename T, bool REV, bool PRESENT>
-__device__ __forceinline__ void wide_v(const wide_rsrc_t (&rb)[5], float* __restrict__ acc, float* __restrict__ lxa,
-                                       int lane) {
+__device__ __forceinline__ void wide_v_role(const ResFwdParams& p, int slot, float* __restrict__ acc,
+                                            float* __restrict__ lxa, int lane) {
   using C = WideCfg<T>;
   constexpr int S = C::S, NP = C::NP, P = C::P, MID = C::MID, R = C::RV, G = C::G;
-  static_assert(R % G == 0 && MID % R == 0, "lookahead slots repeat with the ring");
+  constexpr int RB = S * (int)sizeof(T), PB = S * RB;  // bytes of a row, of a plane
+  static_assert(R % G == 0 && MID % R == 0, "lookahead and ring slots repeat with the halves");
   typedef Pack<T, NP> PK;
   const int col = lane * NP;
   const int voff = col * (int)sizeof(T);
   auto line_of = [](int s) { return REV ? S - 1 - s : s; };
-  auto row_off = [&](int s, int lim) { return s < lim ? line_of(s) * S * (int)sizeof(T) : kWideOob; };
+  auto plane_res = [&](int64_t plane, wide_rsrc_t (&rb)[5]) __attribute__((always_inline)) {
+    const int64_t pof = plane * (S * S);
+    const T* w0 = (const T*)p.w + (int64_t)(slot < 0 ? 0 : slot) * 3 * p.npc + pof;
+    rb[0] = wide_rsrc((const T*)p.x + pof, PB);
+    rb[1] = wide_rsrc((const T*)p.lam + pof, PB);
+    rb[2] = wide_rsrc(w0, PB);
+    rb[3] = wide_rsrc(w0 + p.npc, PB);
+    rb[4] = wide_rsrc(w0 + 2 * p.npc, PB);
+  };
 
-  // ring of R rows: x, lam (first half only) and the three weights
   PK ring[R][5];
-  auto load_row = [&](PK (&slot)[5], int s, bool xl) __attribute__((always_inline)) {
-    if (xl) {
-      const int so = row_off(s, MID);
-      wide_load(slot[0], rb[0], voff, so);
-      wide_load(slot[1], rb[1], voff, so);
+  // row s of a plane (wave order): x and lam in the first half, the weights
+  // throughout; ok = false turns the loads into no-ops
+  auto load_row = [&](PK (&sl)[5], const wide_rsrc_t (&rb)[5], int s, bool ok) __attribute__((always_inline)) {
+    const int so = ok ? line_of(s) * RB : kWideOob;
+    if (s < MID) {
+      wide_load(sl[0], rb[0], voff, so);
+      wide_load(sl[1], rb[1], voff, so);
     }
     if (PRESENT) {
-      const int so = row_off(s, S);
 #pragma unroll
-      for (int m = 2; m < 5; ++m) wide_load(slot[m], rb[m], voff, so);
+      for (int m = 2; m < 5; ++m) wide_load(sl[m], rb[m], voff, so);
     }
   };
+  auto preload = [&](const wide_rsrc_t (&rb)[5]) __attribute__((always_inline)) {
 #pragma unroll
-  for (int k = 0; k < R; ++k) load_row(ring[k], k, true);
+    for (int k = 0; k < R; ++k) load_row(ring[k], rb, k, true);
+  };
 
-  float hp[NP];
+  float lxr[MID][NP], hr[MID][NP], hv[MID][NP], hp[NP];
+  auto first_half = [&](const wide_rsrc_t (&rb)[5]) __attribute__((always_inline)) {
 #pragma unroll
-  for (int q = 0; q < NP; ++q) hp[q] = 0.f;
-
-  // first half: rows this wave reaches first; lam * x and h are stored
-  for (int it = 0; it < MID / R; ++it) {
-#pragma unroll
-    for (int k = 0; k < R; ++k) {
-      const int s = it * R + k;
+    for (int q = 0; q < NP; ++q) hp[q] = 0.f;
+    static_for<0, MID>([&](auto sc) __attribute__((always_inline)) {
+      constexpr int s = decltype(sc)::value, k = s % R;
       float lx[NP], a[NP], b[NP], c[NP];
 #pragma unroll
       for (int q = 0; q < NP; ++q) {
@@ -165,107 +181,143 @@ __device__ __forceinline__ void wide_v(const wide_rsrc_t (&rb)[5], float* __rest
           c[q] = ring[k][4].get(q);
         }
       }
-      load_row(ring[k], s + R, true);
-      float* la = lxa + line_of(s) * P + col;
-      float* ac = acc + line_of(s) * P + col;
+      if (PRESENT || s + R < MID) load_row(ring[k], rb, s + R, true);
 #pragma unroll
-      for (int q = 0; q < NP; ++q) la[q] = lx[q];
+      for (int q = 0; q < NP; ++q) lxr[s][q] = lx[q];
       if (PRESENT) {
         wide_step<NP>(lx, a, b, c, hp);
 #pragma unroll
-        for (int q = 0; q < NP; ++q) ac[q] = hp[q];
-      } else {
-#pragma unroll
-        for (int q = 0; q < NP; ++q) ac[q] = 0.f;
+        for (int q = 0; q < NP; ++q) hr[s][q] = hp[q];
       }
-    }
-  }
-  lds_barrier();  // middle: the other wave's first-half rows are stored
-  if (!PRESENT) return;
-
-  // second half: lam * x and the accumulator from LDS, read G rows ahead
-  // (clamped to the last row at the end of the phase)
-  float la[G][NP], aa[G][NP];
-  auto lds_read = [&](float (&l)[NP], float (&a)[NP], int s) __attribute__((always_inline)) {
-    const int o = line_of(s < S ? s : S - 1) * P + col;
-#pragma unroll
-    for (int q = 0; q < NP; ++q) {
-      l[q] = lxa[o + q];
-      a[q] = acc[o + q];
-    }
+    });
   };
+  // rbn: the next plane (has_next), whose first rows the last steps request
+  auto second_half = [&](const wide_rsrc_t (&rb)[5], const wide_rsrc_t (&rbn)[5], bool has_next)
+                         __attribute__((always_inline)) {
+    float la[G][NP];
+    auto lds_read = [&](float (&l)[NP], int s) __attribute__((always_inline)) {
+      const int o = line_of(s) * P + col;
 #pragma unroll
-  for (int g = 0; g < G; ++g) lds_read(la[g], aa[g], MID + g);
-  for (int it = MID / R; it < S / R; ++it) {
+      for (int q = 0; q < NP; ++q) l[q] = lxa[o + q];
+    };
 #pragma unroll
-    for (int k = 0; k < R; ++k) {
-      const int s = it * R + k, gi = k % G;
-      float lx[NP], av[NP], a[NP], b[NP], c[NP];
+    for (int g = 0; g < G; ++g) lds_read(la[g], MID + g);
+    static_for<MID, S>([&](auto sc) __attribute__((always_inline)) {
+      constexpr int s = decltype(sc)::value, k = s % R, gi = (s - MID) % G;
+      float lx[NP], a[NP], b[NP], c[NP];
 #pragma unroll
       for (int q = 0; q < NP; ++q) {
         lx[q] = la[gi][q];
-        av[q] = aa[gi][q];
         a[q] = ring[k][2].get(q);
         b[q] = ring[k][3].get(q);
         c[q] = ring[k][4].get(q);
       }
-      load_row(ring[k], s + R, false);
-      lds_read(la[gi], aa[gi], s + G);
+      if (s + R < S) load_row(ring[k], rb, s + R, true);
+      else load_row(ring[k], rbn, s + R - S, has_next);
+      if (s + G < S) lds_read(la[gi], s + G);
       wide_step<NP>(lx, a, b, c, hp);
-      float* ac = acc + line_of(s) * P + col;
 #pragma unroll
-      for (int q = 0; q < NP; ++q) ac[q] = av[q] + hp[q];
+      for (int q = 0; q < NP; ++q) hv[s - MID][q] = hp[q];
+    });
+  };
+
+  int64_t plane = blockIdx.x;
+  wide_rsrc_t rb[5];
+  plane_res(plane, rb);
+  preload(rb);
+  for (;;) {
+    first_half(rb);
+    const int64_t nxt = plane + gridDim.x;
+    const bool has_next = nxt < p.planes;
+    wide_rsrc_t rbn[5];
+    plane_res(has_next ? nxt : plane, rbn);
+    lds_barrier();  // B0: the previous plane's epilogue has read acc
+    static_for<0, MID>([&](auto sc) __attribute__((always_inline)) {
+      constexpr int s = decltype(sc)::value;
+      const int o = line_of(s) * P + col;
+#pragma unroll
+      for (int q = 0; q < NP; ++q) {
+        lxa[o + q] = lxr[s][q];
+        acc[o + q] = PRESENT ? hr[s][q] : 0.f;
+      }
+    });
+    lds_barrier();  // B1: lam * x and the first halves are stored
+    if (PRESENT) second_half(rb, rbn, has_next);
+    lds_barrier();  // B2: the horizontal first halves have added to acc
+    if (PRESENT) {
+      static_for<MID, S>([&](auto sc) __attribute__((always_inline)) {
+        constexpr int s = decltype(sc)::value;
+        const int o = line_of(s) * P + col;
+#pragma unroll
+        for (int q = 0; q < NP; ++q) acc[o + q] += hv[s - MID][q];
+      });
     }
+    lds_barrier();  // B3: acc holds everything but the horizontal second halves
+    if (!has_next) break;
+    plane = nxt;
+    static_for<0, 5>([&](auto m) __attribute__((always_inline)) { rb[m] = rbn[m]; });
+    if (!PRESENT) preload(rb);
   }
 }
 
-// Phase H for one wave (the direction is present).  rw: plane resources of
-// w0..w2.  Two register tiles: tile t is consumed from one while tile t + 1
-// arrives in the other, requested as whole 128-byte row segments (a line's
+// Horizontal role (waves 2 and 3): each lane owns two adjacent rows.  The
+// first half of the columns (H1) runs after B1, concurrently with the vertical
+// second halves, adding h to acc; the second half (H2) after B3; then the
+// wave writes y = u * acc for the columns of its second half (final once its
+// own H2 has passed them).  Weights arrive as 128-byte row segments (a line's
 // eight 16-byte pieces in consecutive instructions, so it is fetched into the
-// L1 once) and staggered over tile t's columns, which keeps a steady stream
-// of loads under the arithmetic.  During the last tile the wave requests its
-// epilogue rows of u instead (ru; into ur).
-template <typename T, bool REV>
-__device__ __forceinline__ void wide_h(const wide_rsrc_t (&rw)[3], float* __restrict__ acc,
-                                       const float* __restrict__ lxa, int lane, int wave, wide_rsrc_t ru,
-                                       Pack<T, WideCfg<T>::NP> (&ur)[WideCfg<T>::S / 2]) {
+// L1 once) into two register tiles, the next tile's segments staggered over
+// the current tile's columns; during the last tile the wave requests its
+// rows of u for the epilogue, after it the next plane's first tile.
+template <typename T, bool REV, bool PRESENT>
+__device__ __forceinline__ void wide_h_role(const ResFwdParams& p, int slot, float* __restrict__ acc,
+                                            const float* __restrict__ lxa, int lane) {
   using C = WideCfg<T>;
   constexpr int S = C::S, NP = C::NP, P = C::P, G = C::G;
   constexpr int VE = C::VE, TH = C::TH, NV = C::NV, NTH = C::NTH;
-  constexpr int NL = 3 * NP, GAP = TH / NL;  // row segments per tile, steps between their requests
-  constexpr int UPS = (S / 2 + TH - 1) / TH;  // u rows requested per step of the last tile
+  constexpr int RB = S * (int)sizeof(T), PB = S * RB;
+  constexpr int NL = 3 * NP, GAP = TH / NL;   // row segments per tile, steps between their requests
+  constexpr int NU = S / 2;                   // epilogue instructions (two half rows each)
+  constexpr int UPS = (NU + TH - 1) / TH;     // u requests per step of the last tile
   static_assert(TH % G == 0 && GAP >= 1, "lookahead slots repeat with the tile");
   typedef Pack<T, VE> PK;
+  typedef Pack<T, NP> UK;
   const int row0 = lane * NP;
   auto tile_so = [](int t) { return (REV ? NTH - 1 - t : t) * TH * (int)sizeof(T); };
+  auto plane_res = [&](int64_t plane, wide_rsrc_t (&rw)[3]) __attribute__((always_inline)) {
+    const T* w0 = (const T*)p.w + (int64_t)slot * 3 * p.npc + plane * (S * S);
+#pragma unroll
+    for (int m = 0; m < 3; ++m) rw[m] = wide_rsrc(w0 + m * p.npc, PB);
+  };
+  // epilogue lanes: lanes 0-31 and 32-63 cover two rows, NP columns each, of
+  // this wave's half of the columns
+  const int ec = (REV ? 0 : S / 2) + (lane & 31) * NP, erow = lane >> 5;
+  const int uvoff = (erow * S + ec) * (int)sizeof(T);
 
   PK tile[2][3][NP][NV];
   int voff[NP];
 #pragma unroll
-  for (int q = 0; q < NP; ++q) voff[q] = (row0 + q) * S * (int)sizeof(T);
-  auto load_seg = [&](PK (&tb)[3][NP][NV], int m, int q, int so) __attribute__((always_inline)) {
+  for (int q = 0; q < NP; ++q) voff[q] = (row0 + q) * RB;
+  auto load_seg = [&](PK (&tb)[3][NP][NV], const wide_rsrc_t (&rw)[3], int m, int q, int so)
+                      __attribute__((always_inline)) {
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
       const int v = REV ? NV - 1 - i : i;  // the order the columns are used
       wide_load(tb[m][q][v], rw[m], voff[q], so + v * VE * (int)sizeof(T));
     }
   };
+  auto load_tile0 = [&](const wide_rsrc_t (&rw)[3]) __attribute__((always_inline)) {
 #pragma unroll
-  for (int m = 0; m < 3; ++m)
+    for (int m = 0; m < 3; ++m)
 #pragma unroll
-    for (int q = 0; q < NP; ++q) load_seg(tile[0], m, q, tile_so(0));
-
-  const int uvoff = lane * NP * (int)sizeof(T);
+      for (int q = 0; q < NP; ++q) load_seg(tile[0], rw, m, q, tile_so(0));
+  };
+  UK ur[NU];
   float hp[NP];
-#pragma unroll
-  for (int q = 0; q < NP; ++q) hp[q] = 0.f;
   float la[G][NP], aa[G][NP];
 
-#pragma unroll
-  for (int t = 0; t < NTH; ++t) {
-    const int b = t & 1;
-    if (t == NTH / 2) lds_barrier();  // middle: the other wave's first-half additions are done
+  auto run_tile = [&](auto tc, const wide_rsrc_t (&rw)[3], wide_rsrc_t ru) __attribute__((always_inline)) {
+    constexpr int t = decltype(tc)::value, b = t & 1;
     const int c0 = (REV ? NTH - 1 - t : t) * TH;
     auto lds_read = [&](float (&l)[NP], float (&a)[NP], int e) __attribute__((always_inline)) {
 #pragma unroll
@@ -274,7 +326,7 @@ __device__ __forceinline__ void wide_h(const wide_rsrc_t (&rw)[3], float* __rest
         a[q] = acc[(row0 + q) * P + c0 + e];
       }
     };
-    // lookahead inside the tile only, so it never crosses the middle barrier
+    // lookahead inside the tile only, so it never crosses a barrier
 #pragma unroll
     for (int g = 0; g < G; ++g) lds_read(la[g], aa[g], REV ? TH - 1 - g : g);
 #pragma unroll
@@ -291,12 +343,12 @@ __device__ __forceinline__ void wide_h(const wide_rsrc_t (&rw)[3], float* __rest
         c[q] = tile[b][2][q][v].get(el);
       }
       if (t + 1 < NTH) {
-        if (i % GAP == 0 && i / GAP < NL) load_seg(tile[1 - b], (i / GAP) / NP, (i / GAP) % NP, tile_so(t + 1));
+        if (i % GAP == 0 && i / GAP < NL) load_seg(tile[1 - b], rw, (i / GAP) / NP, (i / GAP) % NP, tile_so(t + 1));
       } else {
 #pragma unroll
         for (int k = 0; k < UPS; ++k) {
           const int r = i * UPS + k;
-          if (r < S / 2) wide_load(ur[r], ru, uvoff, (wave * (S / 2) + r) * S * (int)sizeof(T));
+          if (r < NU) wide_load(ur[r], ru, uvoff, 2 * r * RB);
         }
       }
       if (i + G < TH) lds_read(la[gi], aa[gi], REV ? TH - 1 - (i + G) : i + G);
@@ -304,80 +356,77 @@ __device__ __forceinline__ void wide_h(const wide_rsrc_t (&rw)[3], float* __rest
 #pragma unroll
       for (int q = 0; q < NP; ++q) acc[(row0 + q) * P + c0 + e] = av[q] + hp[q];
     }
+  };
+
+  int64_t plane = blockIdx.x;
+  wide_rsrc_t rw[3];
+  if (PRESENT) {
+    plane_res(plane, rw);
+    load_tile0(rw);
+  }
+  for (;;) {
+    const int64_t pof = plane * (S * S);
+    const int64_t nxt = plane + gridDim.x;
+    const bool has_next = nxt < p.planes;
+    const wide_rsrc_t ru = wide_rsrc((const T*)p.u + pof, PB);
+    lds_barrier();  // B0
+    lds_barrier();  // B1: lam * x and the vertical first halves are in LDS
+#pragma unroll
+    for (int q = 0; q < NP; ++q) hp[q] = 0.f;
+    if (PRESENT) static_for<0, NTH / 2>([&](auto tc) __attribute__((always_inline)) { run_tile(tc, rw, ru); });
+    lds_barrier();  // B2
+    lds_barrier();  // B3: the vertical second halves are added
+    if (PRESENT) {
+      static_for<NTH / 2, NTH>([&](auto tc) __attribute__((always_inline)) { run_tile(tc, rw, ru); });
+      if (has_next) {
+        plane_res(nxt, rw);
+        load_tile0(rw);
+      }
+    } else {
+#pragma unroll
+      for (int r = 0; r < NU; ++r) wide_load(ur[r], ru, uvoff, 2 * r * RB);
+    }
+    // y = u * acc over this wave's half of the columns
+    const wide_rsrc_t ry = wide_rsrc((T*)p.y + pof, PB);
+#pragma unroll
+    for (int r = 0; r < NU; ++r) {
+      const int row = 2 * r + erow;
+      float y[NP];
+#pragma unroll
+      for (int q = 0; q < NP; ++q) y[q] = ur[r].get(q) * acc[row * P + ec + q];
+      wide_store<T, NP>(y, ry, uvoff, 2 * r * RB);
+    }
+    if (!has_next) break;
+    plane = nxt;
   }
 }
 
-// y = u * acc: wave w writes rows [64 w, 64 w + 64), each lane two adjacent
-// columns of a row (whole-row stores, LDS reads without conflicts beyond
-// two-way); u of those rows is already in registers (ur).
 template <typename T>
-__device__ __forceinline__ void wide_epilogue(const Pack<T, WideCfg<T>::NP> (&ur)[WideCfg<T>::S / 2], wide_rsrc_t ry,
-                                              const float* __restrict__ acc, int lane, int wave) {
+__global__ void __launch_bounds__(256, 1) wide_fwd_kernel(ResFwdParams p) {
   using C = WideCfg<T>;
-  constexpr int S = C::S, NP = C::NP, P = C::P;
-  const int col = lane * NP, voff = col * (int)sizeof(T);
-#pragma unroll
-  for (int r = 0; r < S / 2; ++r) {
-    const int row = wave * (S / 2) + r;
-    float y[NP];
-#pragma unroll
-    for (int q = 0; q < NP; ++q) y[q] = ur[r].get(q) * acc[row * P + col + q];
-    wide_store<T, NP>(y, ry, voff, row * S * (int)sizeof(T));
-  }
-}
-
-template <typename T>
-__global__ void __launch_bounds__(128, 1) wide_fwd_kernel(ResFwdParams p) {
-  using C = WideCfg<T>;
-  constexpr int S = C::S, HW = S * S, PB = HW * (int)sizeof(T);  // bytes of one plane of a map
   extern __shared__ float lds[];
   float* acc = lds;
   float* lxa = lds + C::ARR;
-
-  for (int64_t plane = blockIdx.x; plane < p.planes; plane += gridDim.x) {
-    // lane-dependent offsets are rebuilt in every iteration: hoisting the
-    // unrolled loops' addresses out of the plane loop would exhaust the VGPRs
-    int tid = threadIdx.x;
-    asm volatile("" : "+v"(tid));
-    const int lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);  // uniform per wave
-    const int64_t pof = plane * HW;
-    // phase V: wave 0 top-to-bottom, wave 1 bottom-to-top
-    {
-      const int slot = p.slot[wave];
-      const T* w0 = (const T*)p.w + (int64_t)(slot < 0 ? 0 : slot) * 3 * p.npc + pof;
-      const wide_rsrc_t rb[5] = {wide_rsrc((const T*)p.x + pof, PB), wide_rsrc((const T*)p.lam + pof, PB),
-                                 wide_rsrc(w0, PB), wide_rsrc(w0 + p.npc, PB), wide_rsrc(w0 + 2 * p.npc, PB)};
-      if (wave == 0) {
-        if (slot >= 0) wide_v<T, false, true>(rb, acc, lxa, lane);
-        else wide_v<T, false, false>(rb, acc, lxa, lane);
-      } else {
-        if (slot >= 0) wide_v<T, true, true>(rb, acc, lxa, lane);
-        else wide_v<T, true, false>(rb, acc, lxa, lane);
-      }
-    }
-    __syncthreads();
-    // phase H: wave 0 left-to-right, wave 1 right-to-left; each wave's rows of
-    // u for the epilogue arrive during its last tile
-    const wide_rsrc_t ru = wide_rsrc((const T*)p.u + pof, PB);
-    Pack<T, C::NP> ur[S / 2];
-    {
-      const int slot = p.slot[2 + wave];
-      if (slot < 0) {
-        const int uvoff = lane * C::NP * (int)sizeof(T);
-#pragma unroll
-        for (int r = 0; r < S / 2; ++r) wide_load(ur[r], ru, uvoff, (wave * (S / 2) + r) * S * (int)sizeof(T));
-        lds_barrier();  // the middle barrier of the phase
-      } else {
-        const T* w0 = (const T*)p.w + (int64_t)slot * 3 * p.npc + pof;
-        const wide_rsrc_t rw[3] = {wide_rsrc(w0, PB), wide_rsrc(w0 + p.npc, PB), wide_rsrc(w0 + 2 * p.npc, PB)};
-        if (wave == 0) wide_h<T, false>(rw, acc, lxa, lane, wave, ru, ur);
-        else wide_h<T, true>(rw, acc, lxa, lane, wave, ru, ur);
-      }
-    }
-    __syncthreads();
-    wide_epilogue<T>(ur, wide_rsrc((T*)p.y + pof, PB), acc, lane, wave);
-    __syncthreads();  // the next plane overwrites both arrays
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);  // uniform per wave
+  const int slot = p.slot[wave];  // T2B, B2T, L2R, R2L
+  switch (wave) {
+    case 0:
+      if (slot >= 0) wide_v_role<T, false, true>(p, slot, acc, lxa, lane);
+      else wide_v_role<T, false, false>(p, slot, acc, lxa, lane);
+      break;
+    case 1:
+      if (slot >= 0) wide_v_role<T, true, true>(p, slot, acc, lxa, lane);
+      else wide_v_role<T, true, false>(p, slot, acc, lxa, lane);
+      break;
+    case 2:
+      if (slot >= 0) wide_h_role<T, false, true>(p, slot, acc, lxa, lane);
+      else wide_h_role<T, false, false>(p, slot, acc, lxa, lane);
+      break;
+    default:
+      if (slot >= 0) wide_h_role<T, true, true>(p, slot, acc, lxa, lane);
+      else wide_h_role<T, true, false>(p, slot, acc, lxa, lane);
+      break;
   }
 }
 
@@ -403,7 +452,7 @@ hipError_t launch_wide(const ResFwdParams& p, hipStream_t st) {
   if (e != hipSuccess) return e;
   const int64_t cus = wide_cu_count();
   const int64_t grid = p.planes < cus ? p.planes : cus;
-  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(128), C::LDS_BYTES, st, p);
+  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(C::NT), C::LDS_BYTES, st, p);
   return hipGetLastError();
 }
 
