@@ -245,11 +245,23 @@ __device__ __forceinline__ void wide_v_role(const ResFwdParams& p, int slot, flo
     if (PRESENT) second_half(rb, rbn, has_next);
     lds_barrier();  // B2: the horizontal first halves have added to acc
     if (PRESENT) {
-      static_for<MID, S>([&](auto sc) __attribute__((always_inline)) {
-        constexpr int s = decltype(sc)::value;
-        const int o = line_of(s) * P + col;
+      // in batches whose reads are all issued before their writes
+      constexpr int AB = 8;
+      static_for<0, MID / AB>([&](auto bc) __attribute__((always_inline)) {
+        constexpr int b0 = MID + decltype(bc)::value * AB;
+        float t[AB][NP];
+        static_for<0, AB>([&](auto jc) __attribute__((always_inline)) {
+          constexpr int j = decltype(jc)::value;
+          const int o = line_of(b0 + j) * P + col;
 #pragma unroll
-        for (int q = 0; q < NP; ++q) acc[o + q] += hv[s - MID][q];
+          for (int q = 0; q < NP; ++q) t[j][q] = acc[o + q];
+        });
+        static_for<0, AB>([&](auto jc) __attribute__((always_inline)) {
+          constexpr int j = decltype(jc)::value;
+          const int o = line_of(b0 + j) * P + col;
+#pragma unroll
+          for (int q = 0; q < NP; ++q) acc[o + q] = t[j][q] + hv[b0 + j - MID][q];
+        });
       });
     }
     lds_barrier();  // B3: acc holds everything but the horizontal second halves
