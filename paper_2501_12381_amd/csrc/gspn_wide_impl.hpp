@@ -399,15 +399,23 @@ __device__ __forceinline__ void wide_h_role(const ResFwdParams& p, int slot, flo
       for (int r = 0; r < NU; ++r) wide_load(ur[r], ru, uvoff, 2 * r * RB);
     }
     // y = u * acc over this wave's half of the columns
+    // (the reads of a batch of rows are issued before its stores)
     const wide_rsrc_t ry = wide_rsrc((T*)p.y + pof, PB);
+    constexpr int EB = 8;
+    static_for<0, NU / EB>([&](auto bc) __attribute__((always_inline)) {
+      constexpr int r0 = decltype(bc)::value * EB;
+      float y[EB][NP];
 #pragma unroll
-    for (int r = 0; r < NU; ++r) {
-      const int row = 2 * r + erow;
-      float y[NP];
+      for (int j = 0; j < EB; ++j)
 #pragma unroll
-      for (int q = 0; q < NP; ++q) y[q] = ur[r].get(q) * acc[row * P + ec + q];
-      wide_store<T, NP>(y, ry, uvoff, 2 * r * RB);
-    }
+        for (int q = 0; q < NP; ++q) y[j][q] = acc[(2 * (r0 + j) + erow) * P + ec + q];
+#pragma unroll
+      for (int j = 0; j < EB; ++j) {
+#pragma unroll
+        for (int q = 0; q < NP; ++q) y[j][q] *= ur[r0 + j].get(q);
+        wide_store<T, NP>(y[j], ry, uvoff, 2 * (r0 + j) * RB);
+      }
+    });
     if (!has_next) break;
     plane = nxt;
   }
