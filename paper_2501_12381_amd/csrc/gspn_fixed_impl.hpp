@@ -39,6 +39,13 @@ struct FixedCfg {
   static constexpr int RH = 6;                                    // horizontal ring (tiles)
   static constexpr int G = 4;                                     // LDS lookahead
   static constexpr bool ALL_VALID = (S == SEG);
+  // epilogue vectors of u and y: the widest of 16/8/4 bytes whose element
+  // count divides S, used when u and y are aligned for them (ULVL: the vec_y
+  // level this needs); the group's vectors spread over the 128 threads
+  static constexpr int VEU = VLH;
+  static constexpr int ULVL = VEU * (int)sizeof(T) == 16 ? 2 : (VEU * (int)sizeof(T) == 8 ? 1 : 3);  // 3: never
+  static constexpr int NEU = S * (S / VEU);             // vectors per plane
+  static constexpr int KU = (PPW * NEU + 127) / 128;    // vectors per thread
   static constexpr int LDS_BYTES = 2 * PPW * ACC * 4;             // accumulators, then lam * x
   static_assert(S % 2 == 0 && S <= 64, "fixed kernel takes even sizes up to 64");
 };
@@ -184,6 +191,27 @@ fixed_fwd_kernel(ResFwdParams p) {
     }
   }
   __syncthreads();
+  // u of every plane of the group for the epilogue, requested now so that its
+  // latency passes under phase H (planes past the end repeat the last one)
+  constexpr int VEU = C::VEU, NEU = C::NEU, KU = C::KU;
+  const bool uvec = p.vec_y >= C::ULVL;
+  Pack<T, VEU> uv[KU];
+  auto u_elem = [&](int k, int64_t& pi, int& off) __attribute__((always_inline)) {
+    int e = tid + k * 128;
+    e = e < PPW * NEU ? e : PPW * NEU - 1;
+    const int pl = e / NEU, r = (e - pl * NEU) / (S / VEU), c = (e - pl * NEU - r * (S / VEU)) * VEU;
+    pi = g0 + pl < p.planes ? g0 + pl : p.planes - 1;
+    off = r * S + c;
+  };
+  if (uvec) {
+#pragma unroll
+    for (int k = 0; k < KU; ++k) {
+      int64_t pi;
+      int off;
+      u_elem(k, pi, off);
+      uv[k].load((const T*)p.u + pi * HW + off);
+    }
+  }
   // phase H: wave 0 left-to-right, wave 1 right-to-left
   {
     const int slot = p.slot[2 + wave];
@@ -199,6 +227,34 @@ fixed_fwd_kernel(ResFwdParams p) {
   }
   __syncthreads();
 
+  if (uvec) {
+    // y = u * acc: the LDS reads of all the thread's vectors first, then the stores
+    float yv[KU][VEU];
+#pragma unroll
+    for (int k = 0; k < KU; ++k) {
+      int64_t pi;
+      int off;
+      u_elem(k, pi, off);
+      const int e = tid + k * 128 < PPW * NEU ? tid + k * 128 : PPW * NEU - 1;
+      const int pl = e / NEU;
+      const float* ac = lds + pl * C::ACC + (off / S) * C::P + off % S;
+#pragma unroll
+      for (int q = 0; q < VEU; ++q) yv[k][q] = ac[q];
+    }
+#pragma unroll
+    for (int k = 0; k < KU; ++k) {
+      int64_t pi;
+      int off;
+      u_elem(k, pi, off);
+      const int e = tid + k * 128;
+      if (e < PPW * NEU && g0 + e / NEU < p.planes) {
+#pragma unroll
+        for (int q = 0; q < VEU; ++q) yv[k][q] *= uv[k].get(q);
+        stv<VEU>((T*)p.y + pi * HW + off, yv[k]);
+      }
+    }
+    return;
+  }
   for (int pl = 0; pl < PPW; ++pl) {
     const int64_t pi = g0 + pl;
     if (pi >= p.planes) break;
