@@ -10,7 +10,9 @@ Prints one JSON line with the throughput in propagated pixel-channel-directions
 per second (B*C*H*W*n per step / seconds), the roofline position of the
 dominant kernel (algorithmic HBM bytes / its average duration, timed with
 events on the stream it runs on) and the float64 CPU oracle timed on a bounded
-sample of the same workload.
+sample of the same workload.  The timed steps run back to back (warm: inputs
+smaller than the 256 MB last-level cache may partly hit in it); "cold" adds
+single steps each preceded by a 1 GiB read that evicts that cache.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--algo auto|resident|stream|two_pass]
 """
@@ -110,6 +112,9 @@ def main() -> int:
     ap.add_argument("--algo", default="auto", choices=sorted(ALGOS), help="forward kernel family")
     ap.add_argument("--bwd-algo", default="auto", choices=sorted(ALGOS), help="backward kernel family")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cold-reps", type=int, default=5,
+                    help="extra single steps, each after a 1 GiB read that evicts the last-level cache "
+                         "(reported as 'cold' beside the timed, warm steps; 0 = skip)")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="also run the reference copy kernel on this many MiB (for counter runs)")
     args = ap.parse_args()
@@ -172,6 +177,34 @@ def main() -> int:
     fwd_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
     bwd_ms = sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps if wl.backward else 0.0
 
+    # cold steps: a 1 GiB read between steps (outside the events) evicts the
+    # inputs from the 256 MB last-level cache, so each step reads them from HBM.
+    # The flush reads (a reduction), so the lines it leaves are clean and the
+    # step pays no write-back for them; medians over the repetitions
+    cold = None
+    if args.cold_reps > 0:
+        flush = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        sink = torch.empty((), dtype=torch.float32, device=dev)
+        torch.sum(flush, dim=0, out=sink)
+        torch.cuda.synchronize()
+        cev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.cold_reps)]
+        for k in range(args.cold_reps):
+            torch.sum(flush, dim=0, out=sink)
+            step(cev[k])
+        torch.cuda.synchronize()
+        del flush, sink
+
+        def median(v):
+            v = sorted(v)
+            return v[len(v) // 2] if len(v) % 2 else 0.5 * (v[len(v) // 2 - 1] + v[len(v) // 2])
+        c_fwd = median([e[0].elapsed_time(e[1]) for e in cev])
+        c_bwd = median([e[1].elapsed_time(e[2]) for e in cev]) if wl.backward else 0.0
+        c_dom = c_bwd if wl.backward and bwd_ms > fwd_ms else c_fwd
+        d_name = "bwd" if wl.backward and bwd_ms > fwd_ms else "fwd"
+        cold = {"reps": args.cold_reps, "flush_bytes": 1 << 30, "fwd_us": c_fwd * 1e3,
+                "bwd_us": c_bwd * 1e3 if wl.backward else None, "step_us": (c_fwd + c_bwd) * 1e3,
+                "dominant_frac": alg_bytes(wl, d_name) / (c_dom / 1e3) / (HBM_PEAK_GBS * 1e9)}
+
     pcd = wl.B * wl.C * wl.H * wl.W * wl.n_dirs
     value = pcd / (ms_step / 1e3)
     dom = "bwd" if wl.backward and bwd_ms > fwd_ms else "fwd"
@@ -182,7 +215,9 @@ def main() -> int:
     print(f"[bench] {wl.name} algo={args.algo}: step {ms_step * 1e3:.1f} us, fwd {fwd_ms * 1e3:.1f} us "
           f"({alg_bytes(wl, 'fwd') / (fwd_ms / 1e3) / 1e9:.0f} GB/s alg)"
           + (f", bwd {bwd_ms * 1e3:.1f} us ({alg_bytes(wl, 'bwd') / (bwd_ms / 1e3) / 1e9:.0f} GB/s alg)"
-             if wl.backward else ""), file=sys.stderr, flush=True)
+             if wl.backward else "")
+          + (f"; cold fwd {cold['fwd_us']:.1f} us" + (f", bwd {cold['bwd_us']:.1f} us" if wl.backward else "")
+             if cold else ""), file=sys.stderr, flush=True)
 
     cpu = None if args.no_cpu_baseline else cpu_baseline(wl)
     step_bytes = alg_bytes(wl, "fwd") + (alg_bytes(wl, "bwd") if wl.backward else 0)
@@ -209,6 +244,7 @@ def main() -> int:
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "avg_launch_us": dom_ms * 1e3, "alg_bytes_per_launch": alg_bytes(wl, dom)},
         "cpu_baseline": cpu,
+        "cold": cold,
     }
     print(json.dumps(out), flush=True)
     return 0
