@@ -162,6 +162,34 @@ def test_128_planes_per_workgroup_counts(planes):
     assert_close(y, oracle_fwd(inp, 0xF), torch.bfloat16, f"planes {planes}")
 
 
+def offset_copy(t, elems):
+    """Contiguous copy of t starting `elems` elements past the start of its allocation."""
+    buf = torch.empty(t.numel() + elems, dtype=t.dtype, device=t.device)
+    v = buf[elems:].view(t.shape)
+    v.copy_(t)
+    return v
+
+
+@pytest.mark.parametrize("shift", [1, 2, 4])
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32], ids=["bf16", "f32"])
+@pytest.mark.parametrize("S", [16, 28, 56, 128])
+def test_size_specialised_kernels_unaligned_u_y(S, dtype, shift):
+    """u and y only element-aligned (the ABI's requirement): the size-specialised
+    kernels' epilogues take u and y as vectors only when their alignment allows,
+    and 128 x 128 leaves the persistent kernel (it needs 16-byte u and y).
+    Three planes: a partly filled last group for the two-plane-per-wave sizes."""
+    print(f"[fwd] unaligned u/y S={S} {dtype} shift={shift}", flush=True)
+    inp = general_inputs(1, 3, S, S, 0xF, dtype, seed=700 + S + shift)
+    inp["u"] = offset_copy(inp["u"], shift)
+    ref = oracle_fwd(inp, 0xF)
+    for algo in (L.GSPN_ALGO_AUTO, L.GSPN_ALGO_RESIDENT):
+        y = offset_copy(torch.zeros_like(inp["x"]), shift + 1)
+        out = ops.gspn_scan_fwd(inp["x"], inp["w"], inp["lam"], inp["u"], 0xF, algo=algo, y=y)
+        torch.cuda.synchronize()
+        assert out.data_ptr() == y.data_ptr()
+        assert_close(out, ref, dtype, f"S={S} shift={shift} algo={ALGO_NAMES[algo]}")
+
+
 @pytest.mark.parametrize("algo", ALGOS, ids=lambda a: ALGO_NAMES[a])
 def test_single_direction_closed_form(algo):
     """Middle weight 1, others 0: each direction is a cumulative sum of lam*x."""
