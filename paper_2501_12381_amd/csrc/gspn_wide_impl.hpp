@@ -278,9 +278,12 @@ __device__ __forceinline__ void wide_v_role(const ResFwdParams& p, int slot, flo
 // wave writes y = u * acc for the columns of its second half (final once its
 // own H2 has passed them).  Weights arrive as 128-byte row segments (a line's
 // eight 16-byte pieces in consecutive instructions, so it is fetched into the
-// L1 once) into two register tiles, the next tile's segments staggered over
-// the current tile's columns; during the last tile the wave requests its
-// rows of u for the epilogue, after it the next plane's first tile.
+// L1 once) into two register tiles.  The wave's own loads go where the
+// vertical waves are busy with LDS only and the memory is otherwise quiet:
+// tile 1 whole while they store their first halves (B0-B1), u for the
+// epilogue while they add their second halves (B2-B3); tiles after the
+// second are staggered over the current tile's columns, and the next plane's
+// first tile follows the last one.
 template <typename T, bool REV, bool PRESENT>
 __device__ __forceinline__ void wide_h_role(const ResFwdParams& p, int slot, float* __restrict__ acc,
                                             const float* __restrict__ lxa, int lane) {
@@ -290,7 +293,6 @@ __device__ __forceinline__ void wide_h_role(const ResFwdParams& p, int slot, flo
   constexpr int RB = S * (int)sizeof(T), PB = S * RB;
   constexpr int NL = 3 * NP, GAP = TH / NL;   // row segments per tile, steps between their requests
   constexpr int NU = S / 2;                   // epilogue instructions (two half rows each)
-  constexpr int UPS = (NU + TH - 1) / TH;     // u requests per step of the last tile
   static_assert(TH % G == 0 && GAP >= 1, "lookahead slots repeat with the tile");
   typedef Pack<T, VE> PK;
   typedef Pack<T, NP> UK;
@@ -328,7 +330,7 @@ __device__ __forceinline__ void wide_h_role(const ResFwdParams& p, int slot, flo
   float hp[NP];
   float la[G][NP], aa[G][NP];
 
-  auto run_tile = [&](auto tc, const wide_rsrc_t (&rw)[3], wide_rsrc_t ru) __attribute__((always_inline)) {
+  auto run_tile = [&](auto tc, const wide_rsrc_t (&rw)[3]) __attribute__((always_inline)) {
     constexpr int t = decltype(tc)::value, b = t & 1;
     const int c0 = (REV ? NTH - 1 - t : t) * TH;
     auto lds_read = [&](float (&l)[NP], float (&a)[NP], int e) __attribute__((always_inline)) {
@@ -354,14 +356,9 @@ __device__ __forceinline__ void wide_h_role(const ResFwdParams& p, int slot, flo
         bb[q] = tile[b][1][q][v].get(el);
         c[q] = tile[b][2][q][v].get(el);
       }
-      if (t + 1 < NTH) {
+      // tile 1 was requested whole before B1, u before B3
+      if (t >= 1 && t + 1 < NTH) {
         if (i % GAP == 0 && i / GAP < NL) load_seg(tile[1 - b], rw, (i / GAP) / NP, (i / GAP) % NP, tile_so(t + 1));
-      } else {
-#pragma unroll
-        for (int k = 0; k < UPS; ++k) {
-          const int r = i * UPS + k;
-          if (r < NU) wide_load(ur[r], ru, uvoff, 2 * r * RB);
-        }
       }
       if (i + G < TH) lds_read(la[gi], aa[gi], REV ? TH - 1 - (i + G) : i + G);
       wide_step<NP>(lx, a, bb, c, hp);
@@ -382,21 +379,28 @@ __device__ __forceinline__ void wide_h_role(const ResFwdParams& p, int slot, flo
     const bool has_next = nxt < p.planes;
     const wide_rsrc_t ru = wide_rsrc((const T*)p.u + pof, PB);
     lds_barrier();  // B0
+    // the second tile while the vertical waves store their first halves
+    if (PRESENT) {
+#pragma unroll
+      for (int m = 0; m < 3; ++m)
+#pragma unroll
+        for (int q = 0; q < NP; ++q) load_seg(tile[1], rw, m, q, tile_so(1));
+    }
     lds_barrier();  // B1: lam * x and the vertical first halves are in LDS
 #pragma unroll
     for (int q = 0; q < NP; ++q) hp[q] = 0.f;
-    if (PRESENT) static_for<0, NTH / 2>([&](auto tc) __attribute__((always_inline)) { run_tile(tc, rw, ru); });
+    if (PRESENT) static_for<0, NTH / 2>([&](auto tc) __attribute__((always_inline)) { run_tile(tc, rw); });
     lds_barrier();  // B2
+    // u for the epilogue while the vertical waves add their second halves
+#pragma unroll
+    for (int r = 0; r < NU; ++r) wide_load(ur[r], ru, uvoff, 2 * r * RB);
     lds_barrier();  // B3: the vertical second halves are added
     if (PRESENT) {
-      static_for<NTH / 2, NTH>([&](auto tc) __attribute__((always_inline)) { run_tile(tc, rw, ru); });
+      static_for<NTH / 2, NTH>([&](auto tc) __attribute__((always_inline)) { run_tile(tc, rw); });
       if (has_next) {
         plane_res(nxt, rw);
         load_tile0(rw);
       }
-    } else {
-#pragma unroll
-      for (int r = 0; r < NU; ++r) wide_load(ur[r], ru, uvoff, 2 * r * RB);
     }
     // y = u * acc over this wave's half of the columns
     // (the reads of a batch of rows are issued before its stores)
