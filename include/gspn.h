@@ -24,13 +24,29 @@
  *
  *   The backward (Alg. 2) is the exact adjoint for the loss <dy, y>.
  *
+ *   Local GSPN (Sec. 4.1 "Local vs Global GSPN"; App. "CUDA Implementation",
+ *   Alg. 1's groups of kNItems lines): `group_h` > 0 splits the rows into
+ *   groups of group_h consecutive rows, [k*group_h, (k+1)*group_h) (the last
+ *   group may be shorter); T2B and B2T restart from a zero state at the first
+ *   row they visit in each group.  `group_w` does the same for the columns
+ *   and L2R / R2L.  0 (or a value >= the line count) is the global scan.
+ *
+ *   Weight normalisation (Sec. 3.3, Eq. 6), flag GSPN_FLAG_W_LOGITS: w holds
+ *   logits l and the scan uses w_k = sigmoid(l_k) / sum_k' sigmoid(l_k'), the
+ *   sum over the three neighbours, or with GSPN_FLAG_EDGE_RENORM over the
+ *   neighbours that lie on the line (the m_i non-zero entries of row i);
+ *   dw is then the gradient with respect to the logits.
+ *
  * Layouts (all tensors contiguous, element type `dtype`):
  *   x, lam, u, y, dy, dx, dlam, du : (B, C, H, W)
  *   w, dw                          : (n, 3, B, C, H, W), n = popcount(mask), the
  *                                    directions in increasing bit order; w[d][k] is
  *                                    the weight the RECEIVING pixel gives its
  *                                    neighbour k, stored at that pixel's (i, j).
- *   lam and u are shared by all directions.
+ *   lam and u are shared by all directions, and y merges them, unless a
+ *   per-direction flag is set (see GSPN_FLAG_*): then that tensor (and its
+ *   gradient) is (n, B, C, H, W), one map per direction in the same order as
+ *   w, and with GSPN_FLAG_Y_PER_DIR y_d = u_d * h_d is returned unmerged.
  *
  * Arithmetic: inputs are widened to fp32, every sum and product is fp32, and
  * each output element is rounded once (round-to-nearest-even for bf16).
@@ -62,6 +78,15 @@ extern "C" {
 
 typedef enum { GSPN_F32 = 0, GSPN_BF16 = 1 } gspn_dtype;
 
+/* Options of a scan call (the `flags` argument, OR-ed together). */
+enum {
+  GSPN_FLAG_W_LOGITS = 1u,    /* w holds logits, normalised by Eq. 6 inside the call */
+  GSPN_FLAG_EDGE_RENORM = 2u, /* with W_LOGITS: normalise over the on-line neighbours only */
+  GSPN_FLAG_LAM_PER_DIR = 4u, /* lam and dlam are (n, B, C, H, W) */
+  GSPN_FLAG_U_PER_DIR = 8u,   /* u and du are (n, B, C, H, W) */
+  GSPN_FLAG_Y_PER_DIR = 16u   /* y and dy are (n, B, C, H, W): y_d = u_d * h_d, not merged */
+};
+
 enum {
   GSPN_DIR_T2B = 1u, /* top to bottom */
   GSPN_DIR_B2T = 2u, /* bottom to top */
@@ -77,7 +102,8 @@ enum {
   GSPN_ERR_DTYPE = 4,       /* unknown dtype */
   GSPN_ERR_ALIGN = 5,       /* a pointer is not aligned to its element size (workspace: 256 B) */
   GSPN_ERR_ALIAS = 6,       /* an output overlaps an input or another output */
-  GSPN_ERR_UNSUPPORTED = 7, /* H or W above GSPN_MAX_LINE, or a forced algorithm that cannot run */
+  GSPN_ERR_UNSUPPORTED = 7, /* H or W above GSPN_MAX_LINE, unknown flags, EDGE_RENORM without
+                               W_LOGITS, a negative group, or a forced algorithm that cannot run */
   GSPN_ERR_WORKSPACE = 8,   /* workspace NULL or smaller than required */
   GSPN_ERR_HIP = 9          /* a HIP launch or runtime call failed */
 };
@@ -86,8 +112,10 @@ enum {
 #define GSPN_MAX_LINE 4096
 
 /* Algorithm selection (the `algo` argument).  AUTO picks the fastest kernel
- * family for the shape; the others force one family (for testing), and
- * return GSPN_ERR_UNSUPPORTED when it cannot take the shape. */
+ * family for the shape, groups and flags; the others force one family (for
+ * testing), and return GSPN_ERR_UNSUPPORTED when it cannot take the problem.
+ * Every family takes groups; the flags are taken by the streaming family
+ * (AUTO routes a call with flags there). */
 enum {
   GSPN_ALGO_AUTO = 0,
   GSPN_ALGO_RESIDENT = 1, /* whole plane kept on chip, all directions in one kernel */
@@ -104,34 +132,44 @@ enum {
 };
 
 /* Bytes of workspace gspn_scan_fwd needs for this problem (0 if none). */
-size_t gspn_scan_fwd_workspace_bytes(int64_t B, int64_t C, int64_t H, int64_t W,
-                                     uint32_t mask, int dtype, int algo);
+size_t gspn_scan_fwd_workspace_bytes(int64_t B, int64_t C, int64_t H, int64_t W, uint32_t mask,
+                                     gspn_dtype dtype, int64_t group_h, int64_t group_w,
+                                     uint32_t flags, int algo);
 
 /*
  * Forward scan (Eq. 1-2): y = u * sum_{d in mask} h_d.
  *   x, w, lam, u : inputs (see layouts above); y : output, fully overwritten.
+ *   group_h, group_w : local-GSPN group lengths (0 = global), see above.
+ *   flags        : GSPN_FLAG_* options (0 = plain weights, shared lam/u, merged y).
  *   workspace    : device scratch of at least gspn_scan_fwd_workspace_bytes()
  *                  bytes, may be NULL when that size is 0.
  */
 int gspn_scan_fwd(const void* x, const void* w, const void* lam, const void* u, void* y,
-                  int64_t B, int64_t C, int64_t H, int64_t W, uint32_t mask, int dtype,
-                  int algo, void* workspace, size_t workspace_bytes, void* stream);
+                  int64_t B, int64_t C, int64_t H, int64_t W, uint32_t mask, gspn_dtype dtype,
+                  int64_t group_h, int64_t group_w, uint32_t flags, int algo,
+                  void* workspace, size_t workspace_bytes, void* stream);
 
-/* Bytes of workspace gspn_scan_bwd needs for this problem (0 if none). */
-size_t gspn_scan_bwd_workspace_bytes(int64_t B, int64_t C, int64_t H, int64_t W,
-                                     uint32_t mask, int dtype, int algo);
+/* Bytes of workspace gspn_scan_bwd needs for this problem (0 if none).  With
+ * GSPN_ALGO_AUTO the size covers every pointer alignment: AUTO runs the
+ * streaming family, which needs a workspace, when a tensor the resident
+ * kernels would read or write as 16-byte vectors is only element-aligned. */
+size_t gspn_scan_bwd_workspace_bytes(int64_t B, int64_t C, int64_t H, int64_t W, uint32_t mask,
+                                     gspn_dtype dtype, int64_t group_h, int64_t group_w,
+                                     uint32_t flags, int algo);
 
 /*
  * Backward scan (Alg. 2, exact adjoint of Eq. 1-2) for the loss <dy, y>:
- *   inputs dy, x, w, lam, u (same values as the forward call);
- *   outputs dx, dlam, du (B, C, H, W) and dw (n, 3, B, C, H, W), fully
- *   overwritten (not accumulated).  The forward state is recomputed inside,
- *   so no tensor from the forward call is needed.
+ *   inputs dy, x, w, lam, u (same values, groups and flags as the forward call);
+ *   outputs dx, dlam, du and dw (shaped like x, lam, u and w), fully
+ *   overwritten (not accumulated).  With GSPN_FLAG_W_LOGITS dw is the
+ *   gradient with respect to the logits.  The forward state is recomputed
+ *   inside, so no tensor from the forward call is needed.
  */
 int gspn_scan_bwd(const void* dy, const void* x, const void* w, const void* lam, const void* u,
                   void* dx, void* dw, void* dlam, void* du,
-                  int64_t B, int64_t C, int64_t H, int64_t W, uint32_t mask, int dtype,
-                  int algo, void* workspace, size_t workspace_bytes, void* stream);
+                  int64_t B, int64_t C, int64_t H, int64_t W, uint32_t mask, gspn_dtype dtype,
+                  int64_t group_h, int64_t group_w, uint32_t flags, int algo,
+                  void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * Plain device-to-device copy of `bytes` bytes (src and dst 16-byte aligned,

@@ -15,6 +15,9 @@ using namespace gspn;
 namespace {
 
 constexpr size_t kWsAlign = 256;
+// families whose kernels take local-GSPN groups (the streaming family always does)
+constexpr bool kResidentGroups = false;
+constexpr bool kTwoPassGroups = false;
 
 size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
@@ -37,17 +40,34 @@ bool mul_ok(int64_t a, int64_t b, int64_t* out) {
   return true;
 }
 
+constexpr uint32_t kAllFlags = GSPN_FLAG_W_LOGITS | GSPN_FLAG_EDGE_RENORM | GSPN_FLAG_LAM_PER_DIR |
+                               GSPN_FLAG_U_PER_DIR | GSPN_FLAG_Y_PER_DIR;
+
 struct Problem {
   int64_t B, C, H, W, planes, npc;  // npc = elements per (B,C,H,W) tensor
   int n;
   bool empty;
+  int gh, gw;                       // group lengths, 0 when the scan is global on that axis
+  uint32_t flags;
+  bool grouped() const { return gh > 0 || gw > 0; }
+  bool lam_pd() const { return flags & GSPN_FLAG_LAM_PER_DIR; }
+  bool u_pd() const { return flags & GSPN_FLAG_U_PER_DIR; }
+  bool y_pd() const { return flags & GSPN_FLAG_Y_PER_DIR; }
+  bool logits() const { return flags & GSPN_FLAG_W_LOGITS; }
 };
 
-int check_shape(int64_t B, int64_t C, int64_t H, int64_t W, uint32_t mask, int dtype, int algo,
-                Problem* p) {
+int check_shape(int64_t B, int64_t C, int64_t H, int64_t W, uint32_t mask, int dtype, int64_t group_h,
+                int64_t group_w, uint32_t flags, int algo, Problem* p) {
   if (dtype != GSPN_F32 && dtype != GSPN_BF16) return GSPN_ERR_DTYPE;
   if (mask == 0 || mask > 15u) return GSPN_ERR_MASK;
   if (algo < GSPN_ALGO_AUTO || algo > GSPN_ALGO_TWO_PASS) return GSPN_ERR_UNSUPPORTED;
+  if (flags & ~kAllFlags) return GSPN_ERR_UNSUPPORTED;
+  if ((flags & GSPN_FLAG_EDGE_RENORM) && !(flags & GSPN_FLAG_W_LOGITS)) return GSPN_ERR_UNSUPPORTED;
+  if (group_h < 0 || group_w < 0) return GSPN_ERR_UNSUPPORTED;
+  p->flags = flags;
+  // a group at least as long as the axis is the global scan
+  p->gh = (group_h == 0 || group_h >= H) ? 0 : (int)group_h;
+  p->gw = (group_w == 0 || group_w >= W) ? 0 : (int)group_w;
   if (B < 0 || C < 0 || H < 0 || W < 0) return GSPN_ERR_SHAPE;
   p->B = B; p->C = C; p->H = H; p->W = W;
   p->n = popcount4(mask);
@@ -102,9 +122,15 @@ int check_ws(void* ws, size_t ws_bytes, size_t need,
   return GSPN_OK;
 }
 
-bool resident_fits(const Problem& p, int dtype, bool backward);  // defined below
+bool resident_fits(const Problem& p, int dtype, bool backward) {
+  // the flags are implemented by the streaming family only; every family takes groups
+  if (p.flags) return false;
+  if (p.grouped() && !kResidentGroups) return false;
+  return gspn::resident_fits((int)p.H, (int)p.W, dtype, backward);
+}
 
 bool two_pass_fits(const Problem& p, int dtype, bool backward) {
+  if (p.flags || (p.grouped() && !kTwoPassGroups)) return false;
   return !backward && gspn::large_fwd_fits((int)p.H, (int)p.W, dtype);
 }
 
@@ -115,10 +141,6 @@ int choose_algo(const Problem& p, int dtype, int algo, bool backward) {
   if (algo == GSPN_ALGO_TWO_PASS) return two_pass_fits(p, dtype, backward) ? algo : -1;
   if (resident_fits(p, dtype, backward)) return GSPN_ALGO_RESIDENT;
   return two_pass_fits(p, dtype, backward) ? GSPN_ALGO_TWO_PASS : GSPN_ALGO_STREAM;
-}
-
-bool resident_fits(const Problem& p, int dtype, bool backward) {
-  return gspn::resident_fits((int)p.H, (int)p.W, dtype, backward);
 }
 
 // two-pass layout: fp32 partial sums (n > 1; a second array when both vertical
@@ -137,7 +159,7 @@ size_t two_pass_state_bytes(const Problem& p, uint32_t mask) {
 }
 
 size_t fwd_ws_bytes(const Problem& p, int algo, uint32_t mask) {
-  if (algo == GSPN_ALGO_STREAM && p.n > 1) return round_up((size_t)p.npc * 4, kWsAlign);
+  if (algo == GSPN_ALGO_STREAM && p.n > 1 && !p.y_pd()) return round_up((size_t)p.npc * 4, kWsAlign);
   if (algo == GSPN_ALGO_TWO_PASS) return two_pass_acc_bytes(p, mask) + two_pass_state_bytes(p, mask);
   return 0;
 }
@@ -154,30 +176,41 @@ int hip_status(hipError_t e) { return e == hipSuccess ? GSPN_OK : GSPN_ERR_HIP; 
 extern "C" {
 
 size_t gspn_scan_fwd_workspace_bytes(int64_t B, int64_t C, int64_t H, int64_t W, uint32_t mask,
-                                     int dtype, int algo) {
+                                     gspn_dtype dtype, int64_t group_h, int64_t group_w, uint32_t flags,
+                                     int algo) {
   Problem p;
-  if (check_shape(B, C, H, W, mask, dtype, algo, &p) != GSPN_OK || p.empty) return 0;
+  if (check_shape(B, C, H, W, mask, dtype, group_h, group_w, flags, algo, &p) != GSPN_OK || p.empty)
+    return 0;
   const int a = choose_algo(p, dtype, algo, false);
   return a < 0 ? 0 : fwd_ws_bytes(p, a, mask);
 }
 
 size_t gspn_scan_bwd_workspace_bytes(int64_t B, int64_t C, int64_t H, int64_t W, uint32_t mask,
-                                     int dtype, int algo) {
+                                     gspn_dtype dtype, int64_t group_h, int64_t group_w, uint32_t flags,
+                                     int algo) {
   Problem p;
-  if (check_shape(B, C, H, W, mask, dtype, algo, &p) != GSPN_OK || p.empty) return 0;
+  if (check_shape(B, C, H, W, mask, dtype, group_h, group_w, flags, algo, &p) != GSPN_OK || p.empty)
+    return 0;
   const int a = choose_algo(p, dtype, algo, true);
-  return a < 0 ? 0 : bwd_ws_bytes(p, a);
+  if (a < 0) return 0;
+  // AUTO runs the streaming family instead of the resident one when a pointer
+  // is not 16-byte aligned, so its size covers that case too
+  if (algo == GSPN_ALGO_AUTO && (a == GSPN_ALGO_RESIDENT || a == GSPN_ALGO_RESIDENT_GENERIC))
+    return bwd_ws_bytes(p, GSPN_ALGO_STREAM);
+  return bwd_ws_bytes(p, a);
 }
 
 int gspn_scan_fwd(const void* x, const void* w, const void* lam, const void* u, void* y,
-                  int64_t B, int64_t C, int64_t H, int64_t W, uint32_t mask, int dtype, int algo,
+                  int64_t B, int64_t C, int64_t H, int64_t W, uint32_t mask, gspn_dtype dtype,
+                  int64_t group_h, int64_t group_w, uint32_t flags, int algo,
                   void* workspace, size_t workspace_bytes, void* stream) {
   Problem p;
-  int st = check_shape(B, C, H, W, mask, dtype, algo, &p);
+  int st = check_shape(B, C, H, W, mask, dtype, group_h, group_w, flags, algo, &p);
   if (st != GSPN_OK || p.empty) return st;
   const size_t es = esize(dtype);
   const size_t tb = (size_t)p.npc * es, wb = tb * 3 * (size_t)p.n;
-  st = check_ptrs({{x, tb}, {w, wb}, {lam, tb}, {u, tb}}, {{y, tb}}, es);
+  const size_t lb = p.lam_pd() ? tb * p.n : tb, ub = p.u_pd() ? tb * p.n : tb, yb = p.y_pd() ? tb * p.n : tb;
+  st = check_ptrs({{x, tb}, {w, wb}, {lam, lb}, {u, ub}}, {{y, yb}}, es);
   if (st != GSPN_OK) return st;
   int a = choose_algo(p, dtype, algo, false);
   if (a < 0) return GSPN_ERR_UNSUPPORTED;
@@ -191,13 +224,14 @@ int gspn_scan_fwd(const void* x, const void* w, const void* lam, const void* u, 
       }
   }
   const size_t need = fwd_ws_bytes(p, a, mask);
-  st = check_ws(workspace, workspace_bytes, need, {{x, tb}, {w, wb}, {lam, tb}, {u, tb}, {y, tb}});
+  st = check_ws(workspace, workspace_bytes, need, {{x, tb}, {w, wb}, {lam, lb}, {u, ub}, {y, yb}});
   if (st != GSPN_OK) return st;
 
   if (a == GSPN_ALGO_RESIDENT || a == GSPN_ALGO_RESIDENT_GENERIC) {
     ResidentFwdArgs r{};
     r.x = x; r.lam = lam; r.w = w; r.u = u; r.y = y;
     r.mask = mask; r.planes = p.planes; r.H = (int)H; r.W = (int)W; r.dtype = dtype;
+    r.group_h = p.gh; r.group_w = p.gw;
     r.use_fixed = a == GSPN_ALGO_RESIDENT;
     r.stream = stream;
     return hip_status(resident_fwd(r));
@@ -209,21 +243,29 @@ int gspn_scan_fwd(const void* x, const void* w, const void* lam, const void* u, 
     l.acc_b = two_pass_split_v(mask) ? (float*)((char*)workspace + round_up((size_t)p.npc * 4, kWsAlign)) : nullptr;
     l.state = (float*)((char*)workspace + two_pass_acc_bytes(p, mask));
     l.mask = mask; l.planes = p.planes; l.H = (int)H; l.W = (int)W; l.dtype = dtype;
+    l.group_h = p.gh; l.group_w = p.gw;
     l.stream = stream;
     return hip_status(large_fwd(l));
   }
   const std::vector<int> ds = dirs_of(mask);
   const int n = (int)ds.size();
+  const bool merge = n > 1 && !p.y_pd();
   for (int i = 0; i < n; ++i) {
     StreamFwdArgs s{};
-    s.x = x; s.lam = lam; s.u = u; s.y = y;
+    s.x = x;
+    s.lam = (const char*)lam + (p.lam_pd() ? i * tb : 0);
+    s.u = (const char*)u + (p.u_pd() ? i * tb : 0);
+    s.y = (char*)y + (p.y_pd() ? i * tb : 0);
     s.w = (const char*)w + (size_t)i * 3 * tb;
     s.wstride = p.npc;
-    s.acc = n > 1 ? (float*)workspace : nullptr;
+    s.acc = merge ? (float*)workspace : nullptr;
     s.hprev_out = nullptr;
     s.first = i == 0;
-    s.mode = (i == n - 1) ? MODE_FINAL : (i == 0 ? MODE_STORE : MODE_ADD);
+    s.mode = (!merge || i == n - 1) ? MODE_FINAL : (i == 0 ? MODE_STORE : MODE_ADD);
     s.planes = p.planes; s.H = (int)H; s.W = (int)W; s.dir = ds[i]; s.dtype = dtype;
+    s.group = (ds[i] == DIR_T2B || ds[i] == DIR_B2T) ? p.gh : p.gw;
+    s.logits = p.logits(); s.renorm = (flags & GSPN_FLAG_EDGE_RENORM) ? 1 : 0;
+    s.ugate = merge && p.u_pd();
     s.stream = stream;
     st = hip_status(stream_fwd_pass(s));
     if (st != GSPN_OK) return st;
@@ -233,15 +275,16 @@ int gspn_scan_fwd(const void* x, const void* w, const void* lam, const void* u, 
 
 int gspn_scan_bwd(const void* dy, const void* x, const void* w, const void* lam, const void* u,
                   void* dx, void* dw, void* dlam, void* du, int64_t B, int64_t C, int64_t H,
-                  int64_t W, uint32_t mask, int dtype, int algo, void* workspace,
-                  size_t workspace_bytes, void* stream) {
+                  int64_t W, uint32_t mask, gspn_dtype dtype, int64_t group_h, int64_t group_w,
+                  uint32_t flags, int algo, void* workspace, size_t workspace_bytes, void* stream) {
   Problem p;
-  int st = check_shape(B, C, H, W, mask, dtype, algo, &p);
+  int st = check_shape(B, C, H, W, mask, dtype, group_h, group_w, flags, algo, &p);
   if (st != GSPN_OK || p.empty) return st;
   const size_t es = esize(dtype);
   const size_t tb = (size_t)p.npc * es, wb = tb * 3 * (size_t)p.n;
-  st = check_ptrs({{dy, tb}, {x, tb}, {w, wb}, {lam, tb}, {u, tb}},
-                  {{dx, tb}, {dw, wb}, {dlam, tb}, {du, tb}}, es);
+  const size_t lb = p.lam_pd() ? tb * p.n : tb, ub = p.u_pd() ? tb * p.n : tb, yb = p.y_pd() ? tb * p.n : tb;
+  st = check_ptrs({{dy, yb}, {x, tb}, {w, wb}, {lam, lb}, {u, ub}},
+                  {{dx, tb}, {dw, wb}, {dlam, lb}, {du, ub}}, es);
   if (st != GSPN_OK) return st;
   int a = choose_algo(p, dtype, algo, true);
   if (a < 0) return GSPN_ERR_UNSUPPORTED;
@@ -250,13 +293,13 @@ int gspn_scan_bwd(const void* dy, const void* x, const void* w, const void* lam,
     for (const void* q : {dy, x, w, lam, u, (const void*)dx, (const void*)dw, (const void*)dlam, (const void*)du})
       if ((uintptr_t)q % 16) {
         if (algo != GSPN_ALGO_AUTO) return GSPN_ERR_ALIGN;
-        a = GSPN_ALGO_STREAM;  // needs the streaming workspace (size it with GSPN_ALGO_STREAM)
+        a = GSPN_ALGO_STREAM;  // the AUTO workspace size includes this case
         break;
       }
   }
   const size_t need = bwd_ws_bytes(p, a);
   st = check_ws(workspace, workspace_bytes, need,
-                {{dy, tb}, {x, tb}, {w, wb}, {lam, tb}, {u, tb}, {dx, tb}, {dw, wb}, {dlam, tb}, {du, tb}});
+                {{dy, yb}, {x, tb}, {w, wb}, {lam, lb}, {u, ub}, {dx, tb}, {dw, wb}, {dlam, lb}, {du, ub}});
   if (st != GSPN_OK) return st;
 
   if (a == GSPN_ALGO_RESIDENT || a == GSPN_ALGO_RESIDENT_GENERIC) {
@@ -264,6 +307,7 @@ int gspn_scan_bwd(const void* dy, const void* x, const void* w, const void* lam,
     r.dy = dy; r.x = x; r.lam = lam; r.w = w; r.u = u;
     r.dx = dx; r.dw = dw; r.dlam = dlam; r.du = du;
     r.mask = mask; r.planes = p.planes; r.H = (int)H; r.W = (int)W; r.dtype = dtype;
+    r.group_h = p.gh; r.group_w = p.gw;
     r.use_staged = a == GSPN_ALGO_RESIDENT;
     r.stream = stream;
     return hip_status(resident_bwd(r));
@@ -273,35 +317,58 @@ int gspn_scan_bwd(const void* dy, const void* x, const void* w, const void* lam,
   float* hsum = (float*)((char*)workspace + fb);
   float* gsum = (float*)((char*)workspace + 2 * fb);
   const std::vector<int> ds = dirs_of(mask);
+  const bool per_dir = p.lam_pd() || p.u_pd() || p.y_pd();
   for (int i = 0; i < (int)ds.size(); ++i) {
+    const void* dy_i = (const char*)dy + (p.y_pd() ? i * tb : 0);
+    const void* lam_i = (const char*)lam + (p.lam_pd() ? i * tb : 0);
+    const void* u_i = (const char*)u + (p.u_pd() ? i * tb : 0);
+    const int group = (ds[i] == DIR_T2B || ds[i] == DIR_B2T) ? p.gh : p.gw;
     StreamFwdArgs f{};
-    f.x = x; f.lam = lam; f.u = nullptr; f.y = nullptr;
+    f.x = x; f.lam = lam_i; f.u = nullptr; f.y = nullptr;
     f.w = (const char*)w + (size_t)i * 3 * tb;
     f.wstride = p.npc;
     f.acc = hsum;
     f.hprev_out = hprev;
+    if (per_dir && (p.u_pd() || p.y_pd())) {
+      f.dy = dy_i;                                      // hsum (+)= dy_d h, or du_d = dy_d h
+      f.du = p.u_pd() ? (char*)du + i * tb : nullptr;
+      f.hdy = p.u_pd() ? 0 : 1;
+    }
     f.first = i == 0;
     f.mode = MODE_REC;
     f.planes = p.planes; f.H = (int)H; f.W = (int)W; f.dir = ds[i]; f.dtype = dtype;
+    f.group = group;
+    f.logits = p.logits(); f.renorm = (flags & GSPN_FLAG_EDGE_RENORM) ? 1 : 0;
     f.stream = stream;
     st = hip_status(stream_fwd_pass(f));
     if (st != GSPN_OK) return st;
     StreamAdjArgs r{};
-    r.dy = dy; r.u = u;
+    r.dy = dy_i; r.u = u_i;
     r.w = f.w;
     r.wstride = p.npc;
     r.hprev = hprev;
     r.dw = (char*)dw + (size_t)i * 3 * tb;
     r.gsum = gsum;
+    if (p.lam_pd()) {
+      r.lamw = 1;
+      r.lam = lam_i;
+      r.x = x;
+      r.dlam = (char*)dlam + i * tb;
+    }
     r.first = i == 0;
     r.planes = p.planes; r.H = (int)H; r.W = (int)W; r.dir = ds[i]; r.dtype = dtype;
+    r.group = group;
+    r.logits = f.logits; r.renorm = f.renorm;
     r.stream = stream;
     st = hip_status(stream_adj_pass(r));
     if (st != GSPN_OK) return st;
   }
   GradFinishArgs g{};
   g.x = x; g.lam = lam; g.dy = dy; g.gsum = gsum; g.hsum = hsum;
-  g.dx = dx; g.dlam = dlam; g.du = du; g.n = p.npc; g.dtype = dtype; g.stream = stream;
+  g.dx = dx; g.dlam = p.lam_pd() ? nullptr : dlam; g.du = du; g.n = p.npc; g.dtype = dtype;
+  g.dx_mode = p.lam_pd() ? 1 : 0;
+  g.du_mode = p.u_pd() ? 2 : (p.y_pd() ? 1 : 0);
+  g.stream = stream;
   return hip_status(grad_finish(g));
 }
 
@@ -314,13 +381,14 @@ const char* gspn_strerror(int status) {
     case GSPN_ERR_DTYPE: return "unknown dtype";
     case GSPN_ERR_ALIGN: return "misaligned pointer";
     case GSPN_ERR_ALIAS: return "an output overlaps an input or another output";
-    case GSPN_ERR_UNSUPPORTED: return "unsupported: line longer than GSPN_MAX_LINE, too many planes, or forced algorithm cannot run";
+    case GSPN_ERR_UNSUPPORTED: return "unsupported: line longer than GSPN_MAX_LINE, too many planes, unknown flags, "
+                                      "edge renormalisation without logits, negative group, or forced algorithm cannot run";
     case GSPN_ERR_WORKSPACE: return "workspace missing or too small";
     case GSPN_ERR_HIP: return "HIP runtime error";
     default: return "unknown status";
   }
 }
 
-int gspn_version(void) { return 100; }
+int gspn_version(void) { return 200; }
 
 }  // extern "C"

@@ -17,14 +17,20 @@ struct StreamFwdArgs {
   const void* lam;
   const void* w;      // this direction's w0 (w1, w2 follow at +wstride, +2*wstride)
   int64_t wstride;    // elements between the three weight maps (B*C*H*W)
-  const void* u;      // MODE_FINAL only
+  const void* u;      // MODE_FINAL, or every mode with ugate
   float* acc;         // fp32 accumulator (MODE_REC: running sum of h)
   void* y;            // MODE_FINAL only
   float* hprev_out;   // MODE_REC only: h of the previous line, per line
+  const void* dy;     // MODE_REC with per-direction gradients: this direction's dy
+  void* du;           // MODE_REC: du = dy * h written here (per-direction u), or null
   int first;          // MODE_REC: first direction (store instead of add)
   int mode;
   int64_t planes;
   int H, W, dir, dtype;
+  int group;          // lines per local-GSPN group along the scan axis (0: global)
+  int logits, renorm; // w holds logits normalised by Eq. 6 (renorm: on-line neighbours only)
+  int ugate;          // per-direction u: merge u * h instead of h
+  int hdy;            // MODE_REC: hsum accumulates dy * h
   void* stream;
 };
 hipError_t stream_fwd_pass_f32(const StreamFwdArgs& a);
@@ -34,16 +40,22 @@ inline hipError_t stream_fwd_pass(const StreamFwdArgs& a) {
 }
 
 struct StreamAdjArgs {
-  const void* dy;
-  const void* u;
+  const void* dy;     // this direction's dy
+  const void* u;      // this direction's u
   const void* w;
   int64_t wstride;
   const float* hprev;
   void* dw;           // this direction's dw0 (dw1, dw2 at +wstride, +2*wstride)
   float* gsum;
+  const void* lam;    // lamw: this direction's lam
+  const void* x;      // lamw
+  void* dlam;         // lamw: this direction's dlam = x * g
   int first;
   int64_t planes;
   int H, W, dir, dtype;
+  int group;
+  int logits, renorm;
+  int lamw;           // per-direction lam: gsum accumulates lam * g, dlam written here
   void* stream;
 };
 hipError_t stream_adj_pass_f32(const StreamAdjArgs& a);
@@ -59,9 +71,11 @@ struct GradFinishArgs {
   const float* gsum;
   const float* hsum;
   void* dx;
-  void* dlam;
+  void* dlam;         // null when dlam was written per direction
   void* du;
   int64_t n;
+  int dx_mode;        // 0: dx = lam * gsum; 1: dx = gsum
+  int du_mode;        // 0: du = dy * hsum; 1: du = hsum; 2: du written per direction
   int dtype;
   void* stream;
 };
@@ -81,6 +95,7 @@ struct ResidentFwdArgs {
   uint32_t mask;
   int64_t planes;
   int H, W, dtype;
+  int group_h, group_w;  // local-GSPN group lengths (0: global)
   int use_fixed;   // allow the size-specialised kernel when one exists for H x W
   void* stream;
 };
@@ -102,6 +117,7 @@ struct ResidentBwdArgs {
   uint32_t mask;
   int64_t planes;
   int H, W, dtype;
+  int group_h, group_w;  // local-GSPN group lengths (0: global)
   int use_staged;  // allow the LDS-staged kernel for small planes
   void* stream;
 };
@@ -126,6 +142,7 @@ struct LargeFwdArgs {
   uint32_t mask;
   int64_t planes;
   int H, W, dtype;
+  int group_h, group_w;  // local-GSPN group lengths (0: global)
   void* stream;
 };
 hipError_t large_fwd_f32(const LargeFwdArgs& a);

@@ -118,26 +118,81 @@ struct Edges {
   float hi[2][kMaxWaves];  // [parity][wave] value at the wave's last position
 };
 
+// Lines per group and the group-start test (local GSPN): a forward scan
+// enters a group [kG, (k+1)G) at its lowest line, a reverse scan at its
+// highest one; the state is reset to zero there.
+__device__ __forceinline__ bool group_start(int line, int G, bool rev) {
+  return rev ? ((line + 1) % G == 0) : (line % G == 0);
+}
+
+// Eq. 6: the three logits of one pixel -> its three weights (sigmoid, then
+// normalised over the neighbours that count: all three, or with edge
+// renormalisation the ones on the line).  Also returns the sigmoids and the
+// normaliser for the Jacobian of the backward.
+struct Norm3 {
+  float w[3], sg[3], m[3], inv;
+};
+__device__ __forceinline__ Norm3 normalize3(float l0, float l1, float l2, bool first_pos, bool last_pos,
+                                            bool renorm) {
+  Norm3 r;
+  r.sg[0] = 1.f / (1.f + __expf(-l0));
+  r.sg[1] = 1.f / (1.f + __expf(-l1));
+  r.sg[2] = 1.f / (1.f + __expf(-l2));
+  r.m[0] = (renorm && first_pos) ? 0.f : 1.f;
+  r.m[1] = 1.f;
+  r.m[2] = (renorm && last_pos) ? 0.f : 1.f;
+  const float s0 = r.m[0] * r.sg[0], s1 = r.sg[1], s2 = r.m[2] * r.sg[2];
+  r.inv = 1.f / (s0 + s1 + s2);
+  r.w[0] = s0 * r.inv;
+  r.w[1] = s1 * r.inv;
+  r.w[2] = s2 * r.inv;
+  return r;
+}
+
 // ---------------------------------------------------------------------------
 // forward pass of one direction
-//   MODE_STORE: acc = h
-//   MODE_ADD:   acc += h
-//   MODE_FINAL: y = u * (acc + h)   (acc may be null: y = u * h)
-//   MODE_REC:   hprev_out[line] = h of the previous line (0 for the first line),
-//               hsum (+)= h        (recompute step of the backward)
+//   MODE_STORE: acc = h            (ugate: acc = u * h)
+//   MODE_ADD:   acc += h           (ugate: acc += u * h)
+//   MODE_FINAL: y = u * (acc + h)  (ugate: y = acc + u * h; acc may be null)
+//   MODE_REC:   hprev_out[line] = h of the previous line (0 for a group's first
+//               line), hsum (+)= h, or dy * h with hdy; with du: du = dy * h
+//               (recompute step of the backward)
+// EXT enables the per-direction and logit options (runtime flags inside).
 // ---------------------------------------------------------------------------
-template <typename T, bool HZ, bool REV, int NP, int NL, int MODE>
-__global__ void __launch_bounds__(1024)
-stream_fwd_kernel(const T* __restrict__ x, const T* __restrict__ lam, const T* __restrict__ w,
-                  int64_t wstride, const T* __restrict__ u, float* __restrict__ acc,
-                  T* __restrict__ y, float* __restrict__ hprev_out, int first, Geo g,
-                  int vec_ok, int vec_ok_f) {
+struct StreamFwdParams {
+  const void* x;
+  const void* lam;
+  const void* w;
+  int64_t wstride;
+  const void* u;
+  float* acc;
+  void* y;
+  float* hprev_out;
+  const void* dy;
+  void* du;
+  int first;
+  Geo g;
+  int vec_ok, vec_ok_f;
+  int G;       // lines per group (L for the global scan)
+  int logits, renorm, ugate, hdy;
+};
+
+template <typename T, bool HZ, bool REV, int NP, int NL, int MODE, bool EXT>
+__global__ void __launch_bounds__(1024) stream_fwd_kernel(StreamFwdParams p) {
+  const Geo g = p.g;
   const int64_t pbase = (int64_t)blockIdx.x * g.plane;
-  x += pbase; lam += pbase; w += pbase;
-  if (u) u += pbase;
-  if (acc) acc += pbase;
-  if (y) y += pbase;
-  if (hprev_out) hprev_out += pbase;
+  const T* x = (const T*)p.x + pbase;
+  const T* lam = (const T*)p.lam + pbase;
+  const T* w = (const T*)p.w + pbase;
+  const int64_t wstride = p.wstride;
+  const T* u = p.u ? (const T*)p.u + pbase : nullptr;
+  float* acc = p.acc ? p.acc + pbase : nullptr;
+  T* y = p.y ? (T*)p.y + pbase : nullptr;
+  float* hprev_out = p.hprev_out ? p.hprev_out + pbase : nullptr;
+  const T* dyp = (EXT && p.dy) ? (const T*)p.dy + pbase : nullptr;
+  T* dup = (EXT && p.du) ? (T*)p.du + pbase : nullptr;
+  const bool vec_ok = p.vec_ok, vec_ok_f = p.vec_ok_f, first = p.first;
+  const bool ugate = EXT && p.ugate;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = blockDim.x >> 6;
   const int p0 = tid * NP;
   __shared__ Edges ex;
@@ -157,6 +212,19 @@ stream_fwd_kernel(const T* __restrict__ x, const T* __restrict__ lam, const T* _
     load_tile<HZ, NL, NP>(w, g, l0, p0, vec_ok, t0);
     load_tile<HZ, NL, NP>(w + wstride, g, l0, p0, vec_ok, t1);
     load_tile<HZ, NL, NP>(w + 2 * wstride, g, l0, p0, vec_ok, t2);
+    if (EXT && p.logits) {
+#pragma unroll
+      for (int l = 0; l < NL; ++l)
+#pragma unroll
+        for (int q = 0; q < NP; ++q) {
+          const Norm3 r = normalize3(t0[l][q], t1[l][q], t2[l][q], p0 + q == 0, p0 + q == g.P - 1, p.renorm);
+          // positions past the line keep zero weights (their h must stay 0)
+          const bool on = p0 + q < g.P;
+          t0[l][q] = on ? r.w[0] : 0.f;
+          t1[l][q] = on ? r.w[1] : 0.f;
+          t2[l][q] = on ? r.w[2] : 0.f;
+        }
+    }
     if (MODE == MODE_ADD || (MODE == MODE_FINAL && acc) || (MODE == MODE_REC && !first))
       load_tile<HZ, NL, NP>(acc, g, l0, p0, vec_ok_f, to);
     else {
@@ -166,13 +234,19 @@ stream_fwd_kernel(const T* __restrict__ x, const T* __restrict__ lam, const T* _
         for (int q = 0; q < NP; ++q) to[l][q] = 0.f;
     }
     float tu[NL][NP];
-    if (MODE == MODE_FINAL) load_tile<HZ, NL, NP>(u, g, l0, p0, vec_ok, tu);
+    if (MODE == MODE_FINAL || ugate) load_tile<HZ, NL, NP>(u, g, l0, p0, vec_ok, tu);
     float th[NL][NP];  // MODE_REC: previous-line state per line
+    float tdy[NL][NP], tdu[NL][NP];
+    if (EXT && MODE == MODE_REC && dyp) load_tile<HZ, NL, NP>(dyp, g, l0, p0, vec_ok, tdy);
 
 #pragma unroll
     for (int ll = 0; ll < NL; ++ll) {
       const int l = REV ? NL - 1 - ll : ll;
       if (l0 + l < g.L) {  // uniform over the workgroup
+        if (group_start(l0 + l, p.G, REV)) {
+#pragma unroll
+          for (int q = 0; q < NP; ++q) hp[q] = 0.f;
+        }
         if (MODE == MODE_REC) {
 #pragma unroll
           for (int q = 0; q < NP; ++q) th[l][q] = hp[q];
@@ -201,20 +275,29 @@ stream_fwd_kernel(const T* __restrict__ x, const T* __restrict__ lam, const T* _
 #pragma unroll
         for (int q = 0; q < NP; ++q) {
           hp[q] = h[q];
-          to[l][q] += h[q];
+          if (EXT && MODE == MODE_REC && dyp) {
+            const float dh = tdy[l][q] * h[q];
+            tdu[l][q] = dh;
+            to[l][q] += p.hdy ? dh : h[q];
+          } else {
+            to[l][q] += ugate ? tu[l][q] * h[q] : h[q];
+          }
         }
         ++step;
       }
     }
     if (MODE == MODE_FINAL) {
+      if (!ugate) {
 #pragma unroll
-      for (int l = 0; l < NL; ++l)
+        for (int l = 0; l < NL; ++l)
 #pragma unroll
-        for (int q = 0; q < NP; ++q) to[l][q] *= tu[l][q];
+          for (int q = 0; q < NP; ++q) to[l][q] *= tu[l][q];
+      }
       store_tile<HZ, NL, NP>(y, g, l0, p0, vec_ok, to);
     } else {
       store_tile<HZ, NL, NP>(acc, g, l0, p0, vec_ok_f, to);
       if (MODE == MODE_REC) store_tile<HZ, NL, NP>(hprev_out, g, l0, p0, vec_ok_f, th);
+      if (EXT && MODE == MODE_REC && dup) store_tile<HZ, NL, NP>(dup, g, l0, p0, vec_ok, tdu);
     }
   }
 }
@@ -222,17 +305,45 @@ stream_fwd_kernel(const T* __restrict__ x, const T* __restrict__ lam, const T* _
 // ---------------------------------------------------------------------------
 // adjoint pass of one direction (reverse scan order)
 //   g[line][p] = u*dy + sum_k wn_k[p - (k-1)] * gn[p - (k-1)]
-// where gn, wn_k are g and w of the line after this one in scan order.
-//   dw_k[line][p] = g[p] * hprev[line][p + k - 1]
-//   gsum (+)= g
+// where gn, wn_k are g and w of the line after this one in scan order (none
+// when that line starts a group).
+//   dw_k[line][p] = g[p] * hprev[line][p + k - 1]   (logits: through Eq. 6's Jacobian)
+//   gsum (+)= g   (lamw: gsum (+)= lam * g and dlam = x * g)
 // ---------------------------------------------------------------------------
-template <typename T, bool HZ, bool REV, int NP, int NL>
-__global__ void __launch_bounds__(1024)
-stream_adj_kernel(const T* __restrict__ dy, const T* __restrict__ u, const T* __restrict__ w,
-                  int64_t wstride, const float* __restrict__ hprev, T* __restrict__ dw,
-                  float* __restrict__ gsum, int first, Geo g, int vec_ok, int vec_ok_f) {
+struct StreamAdjParams {
+  const void* dy;
+  const void* u;
+  const void* w;
+  int64_t wstride;
+  const float* hprev;
+  void* dw;
+  float* gsum;
+  const void* lam;  // lamw only
+  const void* x;    // lamw only
+  void* dlam;       // lamw only
+  int first;
+  Geo g;
+  int vec_ok, vec_ok_f;
+  int G;
+  int logits, renorm, lamw;
+};
+
+template <typename T, bool HZ, bool REV, int NP, int NL, bool EXT>
+__global__ void __launch_bounds__(1024) stream_adj_kernel(StreamAdjParams p) {
+  const Geo g = p.g;
   const int64_t pbase = (int64_t)blockIdx.x * g.plane;
-  dy += pbase; u += pbase; w += pbase; hprev += pbase; dw += pbase; gsum += pbase;
+  const T* dy = (const T*)p.dy + pbase;
+  const T* u = (const T*)p.u + pbase;
+  const T* w = (const T*)p.w + pbase;
+  const int64_t wstride = p.wstride;
+  const float* hprev = p.hprev + pbase;
+  T* dw = (T*)p.dw + pbase;
+  float* gsum = p.gsum + pbase;
+  const bool lamw = EXT && p.lamw, logits = EXT && p.logits;
+  const T* lamp = lamw ? (const T*)p.lam + pbase : nullptr;
+  const T* xp = lamw ? (const T*)p.x + pbase : nullptr;
+  T* dlamp = lamw ? (T*)p.dlam + pbase : nullptr;
+  const bool vec_ok = p.vec_ok, vec_ok_f = p.vec_ok_f;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = blockDim.x >> 6;
   const int p0 = tid * NP;
   __shared__ Edges ea, eb;  // a: w0*g / w2*g products, b: hprev
@@ -254,19 +365,31 @@ stream_adj_kernel(const T* __restrict__ dy, const T* __restrict__ u, const T* __
     load_tile<HZ, NL, NP>(w + wstride, g, l0, p0, vec_ok, t1);
     load_tile<HZ, NL, NP>(w + 2 * wstride, g, l0, p0, vec_ok, t2);
     load_tile<HZ, NL, NP>(hprev, g, l0, p0, vec_ok_f, th);
-    if (!first) load_tile<HZ, NL, NP>(gsum, g, l0, p0, vec_ok_f, tg);
+    if (!p.first) load_tile<HZ, NL, NP>(gsum, g, l0, p0, vec_ok_f, tg);
     else {
 #pragma unroll
       for (int l = 0; l < NL; ++l)
 #pragma unroll
         for (int q = 0; q < NP; ++q) tg[l][q] = 0.f;
     }
+    float tl[NL][NP], tx[NL][NP], tdl[NL][NP];
+    if (lamw) {
+      load_tile<HZ, NL, NP>(lamp, g, l0, p0, vec_ok, tl);
+      load_tile<HZ, NL, NP>(xp, g, l0, p0, vec_ok, tx);
+    }
     float d0[NL][NP], d1[NL][NP], d2[NL][NP];
 
 #pragma unroll
     for (int ll = 0; ll < NL; ++ll) {
       const int l = adj_rev ? NL - 1 - ll : ll;
-      if (l0 + l < g.L) {
+      const int line = l0 + l;
+      if (line < g.L) {
+        // the line after this one (in scan order) starts a group: it took nothing from here
+        const int nxt = REV ? line - 1 : line + 1;
+        if (nxt >= 0 && nxt < g.L && group_start(nxt, p.G, REV)) {
+#pragma unroll
+          for (int q = 0; q < NP; ++q) gn[q] = 0.f;
+        }
         float a0[NP], a1[NP], a2[NP];
 #pragma unroll
         for (int q = 0; q < NP; ++q) {
@@ -294,14 +417,32 @@ stream_adj_kernel(const T* __restrict__ dy, const T* __restrict__ u, const T* __
           const float gv = tu[l][q] * tdy[l][q] + a1[q] + an + ap;
           const float hl = q == 0 ? h_prev : th[l][q - 1];
           const float hr = q == NP - 1 ? h_next : th[l][q + 1];
-          d0[l][q] = gv * hl;
-          d1[l][q] = gv * th[l][q];
-          d2[l][q] = gv * hr;
-          tg[l][q] += gv;
+          float e0 = gv * hl, e1 = gv * th[l][q], e2 = gv * hr;
+          float c0 = t0[l][q], c1 = t1[l][q], c2 = t2[l][q];
+          if (logits) {
+            const Norm3 r = normalize3(c0, c1, c2, p0 + q == 0, p0 + q == g.P - 1, p.renorm);
+            const float inner = r.w[0] * e0 + r.w[1] * e1 + r.w[2] * e2;
+            e0 = r.m[0] * r.sg[0] * (1.f - r.sg[0]) * (e0 - inner) * r.inv;
+            e1 = r.m[1] * r.sg[1] * (1.f - r.sg[1]) * (e1 - inner) * r.inv;
+            e2 = r.m[2] * r.sg[2] * (1.f - r.sg[2]) * (e2 - inner) * r.inv;
+            const bool on = p0 + q < g.P;  // positions past the line keep zero weights
+            c0 = on ? r.w[0] : 0.f;
+            c1 = on ? r.w[1] : 0.f;
+            c2 = on ? r.w[2] : 0.f;
+          }
+          d0[l][q] = e0;
+          d1[l][q] = e1;
+          d2[l][q] = e2;
+          if (lamw) {
+            tg[l][q] += tl[l][q] * gv;
+            tdl[l][q] = tx[l][q] * gv;
+          } else {
+            tg[l][q] += gv;
+          }
           gn[q] = gv;
-          wn0[q] = t0[l][q];
-          wn1[q] = t1[l][q];
-          wn2[q] = t2[l][q];
+          wn0[q] = c0;
+          wn1[q] = c1;
+          wn2[q] = c2;
         }
         ++step;
       }
@@ -310,21 +451,26 @@ stream_adj_kernel(const T* __restrict__ dy, const T* __restrict__ u, const T* __
     store_tile<HZ, NL, NP>(dw + wstride, g, l0, p0, vec_ok, d1);
     store_tile<HZ, NL, NP>(dw + 2 * wstride, g, l0, p0, vec_ok, d2);
     store_tile<HZ, NL, NP>(gsum, g, l0, p0, vec_ok_f, tg);
+    if (lamw) store_tile<HZ, NL, NP>(dlamp, g, l0, p0, vec_ok, tdl);
   }
 }
 
-// dx = lam * gsum, dlam = x * gsum, du = dy * hsum   (flat, elementwise)
+// dx = lam * gsum (or gsum itself when it already holds sum_d lam_d g_d),
+// dlam = x * gsum (unless written per direction), du = dy * hsum, hsum, or
+// nothing (per-direction du)   (flat, elementwise)
 template <typename T>
 __global__ void __launch_bounds__(256)
 grad_finish_kernel(const T* __restrict__ x, const T* __restrict__ lam, const T* __restrict__ dy,
                    const float* __restrict__ gsum, const float* __restrict__ hsum,
-                   T* __restrict__ dx, T* __restrict__ dlam, T* __restrict__ du, int64_t n) {
+                   T* __restrict__ dx, T* __restrict__ dlam, T* __restrict__ du, int64_t n,
+                   int dx_mode, int du_mode) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
     const float gs = gsum[i];
-    dx[i] = from_f<T>(to_f(lam[i]) * gs);
-    dlam[i] = from_f<T>(to_f(x[i]) * gs);
-    du[i] = from_f<T>(to_f(dy[i]) * hsum[i]);
+    dx[i] = from_f<T>(dx_mode == 0 ? to_f(lam[i]) * gs : gs);
+    if (dlam) dlam[i] = from_f<T>(to_f(x[i]) * gs);
+    if (du_mode == 0) du[i] = from_f<T>(to_f(dy[i]) * hsum[i]);
+    else if (du_mode == 1) du[i] = from_f<T>(hsum[i]);
   }
 }
 
@@ -374,12 +520,10 @@ inline Geo make_geo(int H, int W, int dir) {
   return g;
 }
 
-template <typename T, bool HZ, bool REV, int NP, int MODE>
-hipError_t fwd_np(const StreamFwdArgs& a, const Geo& g, int nw, int vok, int vokf) {
-  hipLaunchKernelGGL((stream_fwd_kernel<T, HZ, REV, NP, nl_for<NP>(), MODE>), dim3((unsigned)a.planes),
-                     dim3(64 * nw), 0, (hipStream_t)a.stream, (const T*)a.x, (const T*)a.lam,
-                     (const T*)a.w, a.wstride, (const T*)a.u, a.acc, (T*)a.y, a.hprev_out, a.first, g,
-                     vok, vokf);
+template <typename T, bool HZ, bool REV, int NP, int MODE, bool EXT>
+hipError_t fwd_np(const StreamFwdParams& p, int64_t planes, int nw, hipStream_t st) {
+  hipLaunchKernelGGL((stream_fwd_kernel<T, HZ, REV, NP, nl_for<NP>(), MODE, EXT>), dim3((unsigned)planes),
+                     dim3(64 * nw), 0, st, p);
   return hipGetLastError();
 }
 
@@ -387,14 +531,25 @@ template <typename T, bool HZ, bool REV, int MODE>
 hipError_t fwd_mode(const StreamFwdArgs& a, const Geo& g) {
   const Shape s = pick_shape(g.P);
   const char* w = (const char*)a.w;
-  const void* in[] = {a.x, a.lam, w, w + a.wstride * sizeof(T), w + 2 * a.wstride * sizeof(T), a.u, a.y};
+  const void* in[] = {a.x, a.lam, w, w + a.wstride * sizeof(T), w + 2 * a.wstride * sizeof(T), a.u, a.y,
+                      a.dy, a.du};
   const void* fp[] = {a.acc, a.hprev_out};
-  const int vok = vec_ok_for(HZ, s.np, 8 / s.np, g.W, in, 7, sizeof(T));
-  const int vokf = vec_ok_for(HZ, s.np, 8 / s.np, g.W, fp, 2, sizeof(float));
+  StreamFwdParams p{};
+  p.x = a.x; p.lam = a.lam; p.w = a.w; p.wstride = a.wstride; p.u = a.u; p.acc = a.acc; p.y = a.y;
+  p.hprev_out = a.hprev_out; p.dy = a.dy; p.du = a.du; p.first = a.first; p.g = g;
+  p.vec_ok = vec_ok_for(HZ, s.np, 8 / s.np, g.W, in, 9, sizeof(T));
+  p.vec_ok_f = vec_ok_for(HZ, s.np, 8 / s.np, g.W, fp, 2, sizeof(float));
+  p.G = (a.group <= 0 || a.group >= g.L) ? g.L : a.group;
+  p.logits = a.logits; p.renorm = a.renorm; p.ugate = a.ugate; p.hdy = a.hdy;
+  const bool ext = a.logits || a.ugate || a.dy != nullptr;
+  hipStream_t st = (hipStream_t)a.stream;
   switch (s.np) {
-    case 1: return fwd_np<T, HZ, REV, 1, MODE>(a, g, s.nw, vok, vokf);
-    case 2: return fwd_np<T, HZ, REV, 2, MODE>(a, g, s.nw, vok, vokf);
-    default: return fwd_np<T, HZ, REV, 4, MODE>(a, g, s.nw, vok, vokf);
+    case 1: return ext ? fwd_np<T, HZ, REV, 1, MODE, true>(p, a.planes, s.nw, st)
+                       : fwd_np<T, HZ, REV, 1, MODE, false>(p, a.planes, s.nw, st);
+    case 2: return ext ? fwd_np<T, HZ, REV, 2, MODE, true>(p, a.planes, s.nw, st)
+                       : fwd_np<T, HZ, REV, 2, MODE, false>(p, a.planes, s.nw, st);
+    default: return ext ? fwd_np<T, HZ, REV, 4, MODE, true>(p, a.planes, s.nw, st)
+                        : fwd_np<T, HZ, REV, 4, MODE, false>(p, a.planes, s.nw, st);
   }
 }
 
@@ -408,11 +563,10 @@ hipError_t fwd_dir(const StreamFwdArgs& a, const Geo& g) {
   }
 }
 
-template <typename T, bool HZ, bool REV, int NP>
-hipError_t adj_np(const StreamAdjArgs& a, const Geo& g, int nw, int vok, int vokf) {
-  hipLaunchKernelGGL((stream_adj_kernel<T, HZ, REV, NP, nl_for<NP>()>), dim3((unsigned)a.planes),
-                     dim3(64 * nw), 0, (hipStream_t)a.stream, (const T*)a.dy, (const T*)a.u,
-                     (const T*)a.w, a.wstride, a.hprev, (T*)a.dw, a.gsum, a.first, g, vok, vokf);
+template <typename T, bool HZ, bool REV, int NP, bool EXT>
+hipError_t adj_np(const StreamAdjParams& p, int64_t planes, int nw, hipStream_t st) {
+  hipLaunchKernelGGL((stream_adj_kernel<T, HZ, REV, NP, nl_for<NP>(), EXT>), dim3((unsigned)planes),
+                     dim3(64 * nw), 0, st, p);
   return hipGetLastError();
 }
 
@@ -422,14 +576,24 @@ hipError_t adj_dir(const StreamAdjArgs& a, const Geo& g) {
   const char* w = (const char*)a.w;
   const char* dw = (const char*)a.dw;
   const void* in[] = {a.dy, a.u, w, w + a.wstride * sizeof(T), w + 2 * a.wstride * sizeof(T), dw,
-                      dw + a.wstride * sizeof(T), dw + 2 * a.wstride * sizeof(T)};
+                      dw + a.wstride * sizeof(T), dw + 2 * a.wstride * sizeof(T), a.lam, a.x, a.dlam};
   const void* fp[] = {a.hprev, a.gsum};
-  const int vok = vec_ok_for(HZ, s.np, 8 / s.np, g.W, in, 8, sizeof(T));
-  const int vokf = vec_ok_for(HZ, s.np, 8 / s.np, g.W, fp, 2, sizeof(float));
+  StreamAdjParams p{};
+  p.dy = a.dy; p.u = a.u; p.w = a.w; p.wstride = a.wstride; p.hprev = a.hprev; p.dw = a.dw;
+  p.gsum = a.gsum; p.lam = a.lam; p.x = a.x; p.dlam = a.dlam; p.first = a.first; p.g = g;
+  p.vec_ok = vec_ok_for(HZ, s.np, 8 / s.np, g.W, in, 11, sizeof(T));
+  p.vec_ok_f = vec_ok_for(HZ, s.np, 8 / s.np, g.W, fp, 2, sizeof(float));
+  p.G = (a.group <= 0 || a.group >= g.L) ? g.L : a.group;
+  p.logits = a.logits; p.renorm = a.renorm; p.lamw = a.lamw;
+  const bool ext = a.logits || a.lamw;
+  hipStream_t st = (hipStream_t)a.stream;
   switch (s.np) {
-    case 1: return adj_np<T, HZ, REV, 1>(a, g, s.nw, vok, vokf);
-    case 2: return adj_np<T, HZ, REV, 2>(a, g, s.nw, vok, vokf);
-    default: return adj_np<T, HZ, REV, 4>(a, g, s.nw, vok, vokf);
+    case 1: return ext ? adj_np<T, HZ, REV, 1, true>(p, a.planes, s.nw, st)
+                       : adj_np<T, HZ, REV, 1, false>(p, a.planes, s.nw, st);
+    case 2: return ext ? adj_np<T, HZ, REV, 2, true>(p, a.planes, s.nw, st)
+                       : adj_np<T, HZ, REV, 2, false>(p, a.planes, s.nw, st);
+    default: return ext ? adj_np<T, HZ, REV, 4, true>(p, a.planes, s.nw, st)
+                        : adj_np<T, HZ, REV, 4, false>(p, a.planes, s.nw, st);
   }
 }
 
@@ -466,7 +630,7 @@ hipError_t grad_finish_t(const GradFinishArgs& a) {
   if (blocks > 65536) blocks = 65536;
   hipLaunchKernelGGL(grad_finish_kernel<T>, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)a.stream,
                      (const T*)a.x, (const T*)a.lam, (const T*)a.dy, a.gsum, a.hsum, (T*)a.dx,
-                     (T*)a.dlam, (T*)a.du, n);
+                     (T*)a.dlam, (T*)a.du, n, a.dx_mode, a.du_mode);
   return hipGetLastError();
 }
 

@@ -16,6 +16,8 @@ GSPN_F32, GSPN_BF16 = 0, 1
 GSPN_DIR_T2B, GSPN_DIR_B2T, GSPN_DIR_L2R, GSPN_DIR_R2L = 1, 2, 4, 8
 GSPN_ALGO_AUTO, GSPN_ALGO_RESIDENT, GSPN_ALGO_STREAM, GSPN_ALGO_RESIDENT_GENERIC = 0, 1, 2, 3
 GSPN_ALGO_TWO_PASS = 4
+GSPN_FLAG_W_LOGITS, GSPN_FLAG_EDGE_RENORM, GSPN_FLAG_LAM_PER_DIR = 1, 2, 4
+GSPN_FLAG_U_PER_DIR, GSPN_FLAG_Y_PER_DIR = 8, 16
 GSPN_MAX_LINE = 4096
 STATUS = {0: "GSPN_OK", 1: "GSPN_ERR_NULL", 2: "GSPN_ERR_SHAPE", 3: "GSPN_ERR_MASK",
           4: "GSPN_ERR_DTYPE", 5: "GSPN_ERR_ALIGN", 6: "GSPN_ERR_ALIAS",
@@ -45,14 +47,16 @@ def load() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
         raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2501_12381_amd.build`")
     lib = ctypes.CDLL(LIB_PATH)
-    lib.gspn_scan_fwd_workspace_bytes.argtypes = [_i64, _i64, _i64, _i64, _u32, _i, _i]
+    ws_args = [_i64, _i64, _i64, _i64, _u32, _i, _i64, _i64, _u32, _i]
+    lib.gspn_scan_fwd_workspace_bytes.argtypes = ws_args
     lib.gspn_scan_fwd_workspace_bytes.restype = _sz
-    lib.gspn_scan_bwd_workspace_bytes.argtypes = [_i64, _i64, _i64, _i64, _u32, _i, _i]
+    lib.gspn_scan_bwd_workspace_bytes.argtypes = ws_args
     lib.gspn_scan_bwd_workspace_bytes.restype = _sz
-    lib.gspn_scan_fwd.argtypes = [_p, _p, _p, _p, _p, _i64, _i64, _i64, _i64, _u32, _i, _i, _p, _sz, _p]
+    lib.gspn_scan_fwd.argtypes = [_p, _p, _p, _p, _p, _i64, _i64, _i64, _i64, _u32, _i, _i64, _i64, _u32,
+                                  _i, _p, _sz, _p]
     lib.gspn_scan_fwd.restype = _i
     lib.gspn_scan_bwd.argtypes = [_p, _p, _p, _p, _p, _p, _p, _p, _p, _i64, _i64, _i64, _i64, _u32,
-                                  _i, _i, _p, _sz, _p]
+                                  _i, _i64, _i64, _u32, _i, _p, _sz, _p]
     lib.gspn_scan_bwd.restype = _i
     lib.gspn_copy_calibration.argtypes = [_p, _p, _sz, _p]
     lib.gspn_copy_calibration.restype = _i
@@ -64,24 +68,28 @@ def load() -> ctypes.CDLL:
     return lib
 
 
-def gspn_scan_fwd_workspace_bytes(B, C, H, W, mask, dtype, algo=GSPN_ALGO_AUTO) -> int:
-    return int(load().gspn_scan_fwd_workspace_bytes(B, C, H, W, mask, dtype, algo))
+def gspn_scan_fwd_workspace_bytes(B, C, H, W, mask, dtype, group_h=0, group_w=0, flags=0,
+                                  algo=GSPN_ALGO_AUTO) -> int:
+    return int(load().gspn_scan_fwd_workspace_bytes(B, C, H, W, mask, dtype, group_h, group_w, flags,
+                                                    algo))
 
 
-def gspn_scan_bwd_workspace_bytes(B, C, H, W, mask, dtype, algo=GSPN_ALGO_AUTO) -> int:
-    return int(load().gspn_scan_bwd_workspace_bytes(B, C, H, W, mask, dtype, algo))
+def gspn_scan_bwd_workspace_bytes(B, C, H, W, mask, dtype, group_h=0, group_w=0, flags=0,
+                                  algo=GSPN_ALGO_AUTO) -> int:
+    return int(load().gspn_scan_bwd_workspace_bytes(B, C, H, W, mask, dtype, group_h, group_w, flags,
+                                                    algo))
 
 
-def gspn_scan_fwd(x, w, lam, u, y, B, C, H, W, mask, dtype, algo, workspace, workspace_bytes,
-                  stream) -> int:
-    return int(load().gspn_scan_fwd(x, w, lam, u, y, B, C, H, W, mask, dtype, algo, workspace,
-                                    workspace_bytes, stream))
-
-
-def gspn_scan_bwd(dy, x, w, lam, u, dx, dw, dlam, du, B, C, H, W, mask, dtype, algo, workspace,
+def gspn_scan_fwd(x, w, lam, u, y, B, C, H, W, mask, dtype, group_h, group_w, flags, algo, workspace,
                   workspace_bytes, stream) -> int:
-    return int(load().gspn_scan_bwd(dy, x, w, lam, u, dx, dw, dlam, du, B, C, H, W, mask, dtype,
+    return int(load().gspn_scan_fwd(x, w, lam, u, y, B, C, H, W, mask, dtype, group_h, group_w, flags,
                                     algo, workspace, workspace_bytes, stream))
+
+
+def gspn_scan_bwd(dy, x, w, lam, u, dx, dw, dlam, du, B, C, H, W, mask, dtype, group_h, group_w, flags,
+                  algo, workspace, workspace_bytes, stream) -> int:
+    return int(load().gspn_scan_bwd(dy, x, w, lam, u, dx, dw, dlam, du, B, C, H, W, mask, dtype,
+                                    group_h, group_w, flags, algo, workspace, workspace_bytes, stream))
 
 
 def gspn_copy_calibration(src, dst, nbytes, stream) -> int:

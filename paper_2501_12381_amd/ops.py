@@ -3,8 +3,18 @@
 Every step of the scan runs in libgspn.so's HIP kernels; torch provides the
 device memory and the current stream.  Tensors must live on a ROCm device:
 there is no CPU path.
+
+Options (keyword arguments, all default off):
+  group_h, group_w : local-GSPN group lengths along the rows (T2B/B2T) and
+                     columns (L2R/R2L); 0 is the global scan;
+  logits, renorm   : w holds logits normalised by Eq. 6 inside the call
+                     (renorm: over the on-line neighbours only);
+  lam_per_dir, u_per_dir, y_per_dir : lam / u / y (and dy) stacked per
+                     direction, shape (n, B, C, H, W).
 """
 from __future__ import annotations
+
+from dataclasses import dataclass
 
 import torch
 
@@ -17,13 +27,35 @@ def n_dirs(mask: int) -> int:
     return bin(mask & 0xF).count("1")
 
 
+@dataclass(frozen=True)
+class ScanOptions:
+    group_h: int = 0
+    group_w: int = 0
+    logits: bool = False
+    renorm: bool = False
+    lam_per_dir: bool = False
+    u_per_dir: bool = False
+    y_per_dir: bool = False
+
+    @property
+    def flags(self) -> int:
+        return ((L.GSPN_FLAG_W_LOGITS if self.logits else 0) | (L.GSPN_FLAG_EDGE_RENORM if self.renorm else 0)
+                | (L.GSPN_FLAG_LAM_PER_DIR if self.lam_per_dir else 0)
+                | (L.GSPN_FLAG_U_PER_DIR if self.u_per_dir else 0)
+                | (L.GSPN_FLAG_Y_PER_DIR if self.y_per_dir else 0))
+
+
 def _dtype_code(t: torch.Tensor) -> int:
     if t.dtype not in _DT:
         raise TypeError(f"GSPN scan supports float32 and bfloat16, got {t.dtype}")
     return _DT[t.dtype]
 
 
-def _check(x, w, lam, u, mask):
+def _shape(base, per_dir: bool, n: int):
+    return ((n,) if per_dir else ()) + tuple(base)
+
+
+def _check(x, w, lam, u, mask, opt: ScanOptions):
     for name, t in (("x", x), ("w", w), ("lam", lam), ("u", u)):
         if not isinstance(t, torch.Tensor):
             raise TypeError(f"{name} must be a tensor")
@@ -35,10 +67,13 @@ def _check(x, w, lam, u, mask):
             raise RuntimeError(f"{name} is on {t.device}, expected {x.device}")
     if x.dim() != 4:
         raise ValueError("x must be (B, C, H, W)")
-    if lam.shape != x.shape or u.shape != x.shape:
-        raise ValueError("lam and u must have the shape of x")
-    if w.shape != (n_dirs(mask), 3) + tuple(x.shape):
-        raise ValueError(f"w must be {(n_dirs(mask), 3) + tuple(x.shape)}, got {tuple(w.shape)}")
+    n = n_dirs(mask)
+    if lam.shape != _shape(x.shape, opt.lam_per_dir, n):
+        raise ValueError(f"lam must be {_shape(x.shape, opt.lam_per_dir, n)}, got {tuple(lam.shape)}")
+    if u.shape != _shape(x.shape, opt.u_per_dir, n):
+        raise ValueError(f"u must be {_shape(x.shape, opt.u_per_dir, n)}, got {tuple(u.shape)}")
+    if w.shape != (n, 3) + tuple(x.shape):
+        raise ValueError(f"w must be {(n, 3) + tuple(x.shape)}, got {tuple(w.shape)}")
 
 
 def _stream(dev) -> int:
@@ -49,45 +84,62 @@ def _ptr(t):
     return t.data_ptr() if t is not None else None
 
 
-def gspn_scan_fwd(x, w, lam, u, mask: int, *, algo: int = L.GSPN_ALGO_AUTO, y=None,
-                  workspace=None) -> torch.Tensor:
+def gspn_scan_fwd(x, w, lam, u, mask: int, *, algo: int = L.GSPN_ALGO_AUTO, y=None, workspace=None,
+                  group_h: int = 0, group_w: int = 0, logits: bool = False, renorm: bool = False,
+                  lam_per_dir: bool = False, u_per_dir: bool = False,
+                  y_per_dir: bool = False) -> torch.Tensor:
     """y = u * sum_{d in mask} h_d (forward line scan of all directions in mask)."""
-    _check(x, w, lam, u, mask)
+    opt = ScanOptions(group_h, group_w, logits, renorm, lam_per_dir, u_per_dir, y_per_dir)
+    _check(x, w, lam, u, mask, opt)
     x, w, lam, u = (t.contiguous() for t in (x, w, lam, u))
     B, C, H, W = x.shape
     dt = _dtype_code(x)
+    yshape = _shape(x.shape, y_per_dir, n_dirs(mask))
     if y is None:
-        y = torch.empty_like(x)
-    elif y.shape != x.shape or y.dtype != x.dtype or not y.is_contiguous():
-        raise ValueError("y must be a contiguous tensor shaped and typed like x")
-    need = L.gspn_scan_fwd_workspace_bytes(B, C, H, W, mask, dt, algo)
+        y = torch.empty(yshape, dtype=x.dtype, device=x.device)
+    elif y.shape != yshape or y.dtype != x.dtype or not y.is_contiguous():
+        raise ValueError(f"y must be a contiguous {x.dtype} tensor of shape {yshape}")
+    need = L.gspn_scan_fwd_workspace_bytes(B, C, H, W, mask, dt, group_h, group_w, opt.flags, algo)
     if workspace is None or workspace.numel() < need:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
     with torch.cuda.device(x.device):
         st = L.gspn_scan_fwd(_ptr(x), _ptr(w), _ptr(lam), _ptr(u), _ptr(y), B, C, H, W, mask, dt,
-                             algo, _ptr(workspace), workspace.numel(), _stream(x.device))
+                             group_h, group_w, opt.flags, algo, _ptr(workspace), workspace.numel(),
+                             _stream(x.device))
     if st != 0:
         raise L.GSPNError(st, "gspn_scan_fwd")
     return y
 
 
-def gspn_scan_bwd(dy, x, w, lam, u, mask: int, *, algo: int = L.GSPN_ALGO_AUTO, workspace=None):
-    """Gradients (dx, dw, dlam, du) of <dy, y> for the forward above."""
-    _check(x, w, lam, u, mask)
-    if dy.shape != x.shape or dy.dtype != x.dtype or dy.device != x.device:
-        raise ValueError("dy must be shaped, typed and placed like x")
+def gspn_scan_bwd(dy, x, w, lam, u, mask: int, *, algo: int = L.GSPN_ALGO_AUTO, workspace=None,
+                  out=None, group_h: int = 0, group_w: int = 0, logits: bool = False,
+                  renorm: bool = False, lam_per_dir: bool = False, u_per_dir: bool = False,
+                  y_per_dir: bool = False):
+    """Gradients (dx, dw, dlam, du) of <dy, y> for the forward above.
+
+    `out` = (dx, dw, dlam, du): optional contiguous output tensors (else new ones)."""
+    opt = ScanOptions(group_h, group_w, logits, renorm, lam_per_dir, u_per_dir, y_per_dir)
+    _check(x, w, lam, u, mask, opt)
+    if dy.shape != _shape(x.shape, y_per_dir, n_dirs(mask)) or dy.dtype != x.dtype or dy.device != x.device:
+        raise ValueError("dy must be shaped like y, typed and placed like x")
     dy, x, w, lam, u = (t.contiguous() for t in (dy, x, w, lam, u))
     B, C, H, W = x.shape
     dt = _dtype_code(x)
-    dx, dlam, du, dw = (torch.empty_like(x), torch.empty_like(x), torch.empty_like(x),
-                        torch.empty_like(w))
-    need = L.gspn_scan_bwd_workspace_bytes(B, C, H, W, mask, dt, algo)
+    if out is None:
+        dx, dlam, du, dw = (torch.empty_like(x), torch.empty_like(lam), torch.empty_like(u),
+                            torch.empty_like(w))
+    else:
+        dx, dw, dlam, du = out
+        for t, ref in ((dx, x), (dw, w), (dlam, lam), (du, u)):
+            if t.shape != ref.shape or t.dtype != x.dtype or t.device != x.device or not t.is_contiguous():
+                raise ValueError("out tensors must be contiguous and shaped like (x, w, lam, u)")
+    need = L.gspn_scan_bwd_workspace_bytes(B, C, H, W, mask, dt, group_h, group_w, opt.flags, algo)
     if workspace is None or workspace.numel() < need:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
     with torch.cuda.device(x.device):
         st = L.gspn_scan_bwd(_ptr(dy), _ptr(x), _ptr(w), _ptr(lam), _ptr(u), _ptr(dx), _ptr(dw),
-                             _ptr(dlam), _ptr(du), B, C, H, W, mask, dt, algo, _ptr(workspace),
-                             workspace.numel(), _stream(x.device))
+                             _ptr(dlam), _ptr(du), B, C, H, W, mask, dt, group_h, group_w, opt.flags,
+                             algo, _ptr(workspace), workspace.numel(), _stream(x.device))
     if st != 0:
         raise L.GSPNError(st, "gspn_scan_bwd")
     return dx, dw, dlam, du
@@ -97,21 +149,22 @@ class GSPNScan(torch.autograd.Function):
     """Autograd wrapper: forward and backward both run the HIP kernels."""
 
     @staticmethod
-    def forward(ctx, x, w, lam, u, mask: int, algo: int = L.GSPN_ALGO_AUTO):
-        ctx.mask, ctx.algo = mask, algo
+    def forward(ctx, x, w, lam, u, mask: int, algo: int = L.GSPN_ALGO_AUTO, opt: ScanOptions = ScanOptions()):
+        ctx.mask, ctx.algo, ctx.opt = mask, algo, opt
         ctx.save_for_backward(x, w, lam, u)
-        return gspn_scan_fwd(x, w, lam, u, mask, algo=algo)
+        return gspn_scan_fwd(x, w, lam, u, mask, algo=algo, **opt.__dict__)
 
     @staticmethod
     def backward(ctx, dy):
         x, w, lam, u = ctx.saved_tensors
-        dx, dw, dlam, du = gspn_scan_bwd(dy.contiguous(), x, w, lam, u, ctx.mask, algo=ctx.algo)
-        return dx, dw, dlam, du, None, None
+        dx, dw, dlam, du = gspn_scan_bwd(dy.contiguous(), x, w, lam, u, ctx.mask, algo=ctx.algo,
+                                         **ctx.opt.__dict__)
+        return dx, dw, dlam, du, None, None, None
 
 
-def gspn_scan(x, w, lam, u, mask: int = 0xF, algo: int = L.GSPN_ALGO_AUTO) -> torch.Tensor:
-    """Differentiable 4-direction (or masked) GSPN line scan."""
-    return GSPNScan.apply(x, w, lam, u, mask, algo)
+def gspn_scan(x, w, lam, u, mask: int = 0xF, algo: int = L.GSPN_ALGO_AUTO, **options) -> torch.Tensor:
+    """Differentiable 4-direction (or masked) GSPN line scan; `options` as in ScanOptions."""
+    return GSPNScan.apply(x, w, lam, u, mask, algo, ScanOptions(**options))
 
 
 def gspn_copy_calibration(src: torch.Tensor, dst: torch.Tensor) -> None:

@@ -150,3 +150,35 @@ def random_general(shape, n_dirs: int, device="cpu", seed: int = 0, dtype=torch.
     w = w / (w.abs().sum(dim=1, keepdim=True) + 0.05)
     dy = torch.randn(shape, generator=g, device=device)
     return {k: v.to(dtype) for k, v in dict(x=x, lam=lam, u=u, w=w, dy=dy).items()}
+
+
+def numpy_planes(wl: Workload, planes: int, seed: int = 0) -> dict:
+    """`planes` planes of the workload's distributions as float64 NumPy arrays
+    (B = 1, C = planes), drawn with NumPy instead of torch.
+
+    For CPU timing runs in worker processes that must not use torch: same
+    shapes and distributions as make_inputs (the values differ, and they are
+    not rounded to the workload dtype).
+    """
+    import numpy as np
+
+    rng = np.random.default_rng([wl.seed, seed, planes])
+    shape = (1, planes, wl.H, wl.W)
+
+    def draw(kind):
+        if kind == "normal":
+            return rng.standard_normal(shape)
+        if kind == "uniform":
+            return rng.random(shape)
+        if kind == "sigmoid":
+            return 1.0 / (1.0 + np.exp(-rng.standard_normal(shape)))
+        if kind == "ones":
+            return np.ones(shape)
+        raise ValueError(kind)
+
+    out = {"x": draw(wl.x), "lam": draw(wl.lam), "u": draw(wl.u)}
+    logits = rng.standard_normal((wl.n_dirs, 3) + shape) * wl.w_logit_std
+    e = np.exp(logits - logits.max(axis=1, keepdims=True))
+    out["w"] = e / e.sum(axis=1, keepdims=True)
+    out["dy"] = rng.standard_normal(shape) if wl.backward else None
+    return out

@@ -44,7 +44,9 @@ def test_header_constants_match_binding():
     consts = dict(re.findall(r"\b(GSPN_[A-Z0-9_]+)\s*=\s*(\d+)u?", src))
     for name in ("GSPN_F32", "GSPN_BF16", "GSPN_DIR_T2B", "GSPN_DIR_B2T", "GSPN_DIR_L2R",
                  "GSPN_DIR_R2L", "GSPN_ALGO_AUTO", "GSPN_ALGO_RESIDENT", "GSPN_ALGO_STREAM",
-                 "GSPN_ALGO_RESIDENT_GENERIC", "GSPN_ALGO_TWO_PASS"):
+                 "GSPN_ALGO_RESIDENT_GENERIC", "GSPN_ALGO_TWO_PASS", "GSPN_FLAG_W_LOGITS",
+                 "GSPN_FLAG_EDGE_RENORM", "GSPN_FLAG_LAM_PER_DIR", "GSPN_FLAG_U_PER_DIR",
+                 "GSPN_FLAG_Y_PER_DIR"):
         assert int(consts[name]) == getattr(L, name), name
     for code, name in L.STATUS.items():
         assert int(consts[name]) == code, name
@@ -56,7 +58,7 @@ def test_strerror_and_version(lib):
         s = L.gspn_strerror(code)
         assert isinstance(s, str) and s
     assert L.gspn_strerror(0) == "success"
-    assert L.gspn_version() >= 100
+    assert L.gspn_version() >= 200
 
 
 def test_workspace_sizes():
@@ -64,33 +66,33 @@ def test_workspace_sizes():
     S = L.GSPN_ALGO_STREAM
     npc = 2 * 3 * 5 * 7
     # streaming forward: one fp32 accumulator when several directions are merged
-    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 7, 0x1, f32, S) == 0
-    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 7, 0xF, bf, S) >= npc * 4
-    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 7, 0xF, bf, S) % 256 == 0
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 7, 0x1, f32, algo=S) == 0
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 7, 0xF, bf, algo=S) >= npc * 4
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 7, 0xF, bf, algo=S) % 256 == 0
     # streaming backward: previous-line state, sum of h, sum of g (fp32 each)
-    assert L.gspn_scan_bwd_workspace_bytes(2, 3, 5, 7, 0xF, f32, S) >= 3 * npc * 4
+    assert L.gspn_scan_bwd_workspace_bytes(2, 3, 5, 7, 0xF, f32, algo=S) >= 3 * npc * 4
     # two-pass forward: fp32 partial sums (several directions; two arrays when
     # both vertical directions feed a horizontal pass), then the column state of
     # the horizontal pass (2 parities x 2 directions x planes x H floats)
     T = L.GSPN_ALGO_TWO_PASS
     acc, state = 2 * 3 * 5 * 64 * 4, 512  # 7680 is a multiple of 256; 4*6*5*4 = 480 -> 512
-    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 64, 0xF, bf, T) == 2 * acc + state
-    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 64, 0x7, bf, T) == 2 * acc + state
-    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 64, 0xD, bf, T) == acc + state
-    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 64, 0x3, bf, T) == acc
-    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 64, 0x4, bf, T) == state
-    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 64, 0x1, bf, T) == 0
-    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 60, 0xF, bf, T) == 0  # W*2 not a multiple of 16
-    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 56, 0xF, bf, T) == 0  # row under 128 bytes
-    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 32, 0xF, f32, T) == 2 * (2 * 3 * 5 * 32 * 4) + 512
-    assert L.gspn_scan_bwd_workspace_bytes(2, 3, 5, 64, 0xF, bf, T) == 0  # forward only
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 64, 0xF, bf, algo=T) == 2 * acc + state
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 64, 0x7, bf, algo=T) == 2 * acc + state
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 64, 0xD, bf, algo=T) == acc + state
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 64, 0x3, bf, algo=T) == acc
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 64, 0x4, bf, algo=T) == state
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 64, 0x1, bf, algo=T) == 0
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 60, 0xF, bf, algo=T) == 0  # W*2 not a multiple of 16
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 56, 0xF, bf, algo=T) == 0  # row under 128 bytes
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 32, 0xF, f32, algo=T) == 2 * (2 * 3 * 5 * 32 * 4) + 512
+    assert L.gspn_scan_bwd_workspace_bytes(2, 3, 5, 64, 0xF, bf, algo=T) == 0  # forward only
     # AUTO takes the two-pass kernels for planes that do not fit on chip
-    big = L.gspn_scan_fwd_workspace_bytes(1, 2, 2048, 2048, 0xF, bf, L.GSPN_ALGO_AUTO)
+    big = L.gspn_scan_fwd_workspace_bytes(1, 2, 2048, 2048, 0xF, bf, algo=L.GSPN_ALGO_AUTO)
     assert big == 2 * (2 * 2048 * 2048 * 4) + 4 * 2 * 2048 * 4
     # invalid problems report 0
-    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 7, 0, f32, S) == 0
-    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 7, 1, 7, S) == 0
-    assert L.gspn_scan_fwd_workspace_bytes(0, 3, 5, 7, 0xF, f32, S) == 0
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 7, 0, f32, algo=S) == 0
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 7, 1, 7, algo=S) == 0
+    assert L.gspn_scan_fwd_workspace_bytes(0, 3, 5, 7, 0xF, f32, algo=S) == 0
 
 
 FAKE = 1 << 40  # never dereferenced: every call below fails validation first
@@ -109,8 +111,9 @@ def _no_gpu():
 
 def fwd(x=FAKE, w=FAKE + (1 << 30), lam=FAKE + (2 << 30), u=FAKE + (3 << 30), y=FAKE + (4 << 30),
         B=1, C=2, H=8, W=8, mask=0xF, dtype=L.GSPN_F32, algo=L.GSPN_ALGO_STREAM, ws=FAKE + (5 << 30),
-        ws_bytes=1 << 20):
-    return L.gspn_scan_fwd(x, w, lam, u, y, B, C, H, W, mask, dtype, algo, ws, ws_bytes, None)
+        ws_bytes=1 << 20, group_h=0, group_w=0, flags=0):
+    return L.gspn_scan_fwd(x, w, lam, u, y, B, C, H, W, mask, dtype, group_h, group_w, flags, algo, ws,
+                           ws_bytes, None)
 
 
 def test_fwd_rejects_bad_arguments(lib):
@@ -136,6 +139,19 @@ def test_fwd_rejects_bad_arguments(lib):
     assert fwd(algo=L.GSPN_ALGO_TWO_PASS) == 7  # 8 fp32 columns: row under 128 bytes
     # the two-pass kernels need 16-byte aligned tensors when forced
     assert fwd(algo=L.GSPN_ALGO_TWO_PASS, W=64, dtype=L.GSPN_BF16, x=FAKE + 2) == 5
+    # options: unknown flags, edge renormalisation without logits, negative groups
+    assert fwd(flags=32) == 7
+    assert fwd(flags=L.GSPN_FLAG_EDGE_RENORM) == 7
+    assert fwd(group_h=-1) == 7
+    assert fwd(group_w=-2) == 7
+    # the flags run in the streaming family only: forcing another family is refused
+    assert fwd(algo=L.GSPN_ALGO_RESIDENT, flags=L.GSPN_FLAG_W_LOGITS) == 7
+    assert fwd(algo=L.GSPN_ALGO_TWO_PASS, W=64, dtype=L.GSPN_BF16, flags=L.GSPN_FLAG_Y_PER_DIR) == 7
+    # per-direction maps are n times larger: y (4 maps of 512 bytes) overlaps u's
+    # second map, lam's fourth map reaches into y
+    assert fwd(flags=L.GSPN_FLAG_U_PER_DIR, y=FAKE + (3 << 30) + 512) == 6
+    assert fwd(flags=L.GSPN_FLAG_LAM_PER_DIR, lam=FAKE + (4 << 30) - 2048 + 64) == 6
+    assert fwd(flags=L.GSPN_FLAG_Y_PER_DIR, y=FAKE - 1024) == 6  # 4 maps of y reach into x
 
 
 def test_empty_problem_is_a_noop(lib):
@@ -153,12 +169,12 @@ def test_bwd_rejects_bad_arguments(lib):
         p = dict(zip(["dy", "x", "w", "lam", "u", "dx", "dw", "dlam", "du", "ws"], base))
         p.update({k: v for k, v in kw.items() if k in p})
         dims = dict(B=1, C=2, H=8, W=8, mask=0xF, dtype=L.GSPN_F32, algo=L.GSPN_ALGO_STREAM,
-                    ws_bytes=1 << 24)
+                    ws_bytes=1 << 24, group_h=0, group_w=0, flags=0)
         dims.update({k: v for k, v in kw.items() if k in dims})
         return L.gspn_scan_bwd(p["dy"], p["x"], p["w"], p["lam"], p["u"], p["dx"], p["dw"],
                                p["dlam"], p["du"], dims["B"], dims["C"], dims["H"], dims["W"],
-                               dims["mask"], dims["dtype"], dims["algo"], p["ws"],
-                               dims["ws_bytes"], None)
+                               dims["mask"], dims["dtype"], dims["group_h"], dims["group_w"],
+                               dims["flags"], dims["algo"], p["ws"], dims["ws_bytes"], None)
 
     assert bwd(mask=0) == 3
     assert bwd(dtype=5) == 4
@@ -167,3 +183,37 @@ def test_bwd_rejects_bad_arguments(lib):
     assert bwd(dx=base[0] + 128) == 6  # dx inside dy
     assert bwd(ws_bytes=100) == 8
     assert bwd(W=-3) == 2
+    assert bwd(flags=64) == 7
+    assert bwd(group_w=-1) == 7
+    assert bwd(flags=L.GSPN_FLAG_Y_PER_DIR, dx=base[0] + 1024) == 6  # dy holds 4 maps: dx inside it
+
+
+def test_bwd_auto_workspace_covers_element_aligned_pointers():
+    """AUTO falls back from the resident backward (16-byte vectors) to the
+    streaming family when a tensor is only element-aligned; the AUTO size must
+    cover that fallback for every shape the resident kernels take."""
+    A, S = L.GSPN_ALGO_AUTO, L.GSPN_ALGO_STREAM
+    for dt in (L.GSPN_F32, L.GSPN_BF16):
+        for side in (16, 28, 32, 56, 64):
+            for mask in (1, 5, 12, 15):
+                auto = L.gspn_scan_bwd_workspace_bytes(2, 3, side, side, mask, dt, algo=A)
+                stream = L.gspn_scan_bwd_workspace_bytes(2, 3, side, side, mask, dt, algo=S)
+                assert stream > 0 and auto >= stream, (dt, side, mask, auto, stream)
+
+
+def test_workspace_sizes_with_options():
+    f32, bf = L.GSPN_F32, L.GSPN_BF16
+    A = L.GSPN_ALGO_AUTO
+    npc4 = 2 * 3 * 5 * 7 * 4
+    # unmerged outputs need no accumulator
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 7, 0xF, f32, flags=L.GSPN_FLAG_Y_PER_DIR, algo=A) == 0
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 7, 0xF, f32, flags=L.GSPN_FLAG_U_PER_DIR, algo=A) >= npc4
+    # flags and groups run in the streaming family: its sizes
+    assert L.gspn_scan_bwd_workspace_bytes(2, 3, 5, 7, 0xF, bf, flags=L.GSPN_FLAG_W_LOGITS, algo=A) >= 3 * npc4
+    # a group at least as long as the axis is the global scan (same family, same size)
+    for g in (0, 5, 6, 100):
+        assert (L.gspn_scan_fwd_workspace_bytes(1, 2, 5, 64, 0xF, bf, group_h=g, algo=A)
+                == L.gspn_scan_fwd_workspace_bytes(1, 2, 5, 64, 0xF, bf, algo=A))
+    # invalid options report 0
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 7, 0xF, f32, flags=1 << 7, algo=A) == 0
+    assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 7, 0xF, f32, group_h=-1, algo=A) == 0

@@ -121,6 +121,34 @@ def test_bwd_deterministic(algo):
         assert torch.equal(u.view(torch.int16), v.view(torch.int16))
 
 
+def offset_copy(t, elems):
+    """Contiguous copy of t starting `elems` elements past the start of its allocation."""
+    buf = torch.empty(t.numel() + elems, dtype=t.dtype, device=t.device)
+    v = buf[elems:].view(t.shape)
+    v.copy_(t)
+    return v
+
+
+@pytest.mark.parametrize("shift", [1, 2, 4])
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16], ids=["f32", "bf16"])
+@pytest.mark.parametrize("S", [16, 28, 32, 56, 64])
+def test_bwd_element_aligned_views(S, dtype, shift):
+    """Every input and output only element-aligned, workspace sized by AUTO:
+    the call must succeed (the resident kernels' vector accesses need 16-byte
+    alignment, so AUTO runs another family) and match the oracle."""
+    print(f"[bwd] element-aligned views S={S} {dtype} shift={shift}", flush=True)
+    t = synth.random_general((1, 3, S, S), 4, device=DEV, seed=900 + S + shift)
+    inp = {k: offset_copy(v.to(dtype), shift) for k, v in t.items()}
+    outs = (offset_copy(torch.zeros_like(inp["x"]), shift + 1),
+            offset_copy(torch.zeros_like(inp["w"]), shift + 1),
+            offset_copy(torch.zeros_like(inp["x"]), shift + 2),
+            offset_copy(torch.zeros_like(inp["x"]), shift + 3))
+    got = ops.gspn_scan_bwd(inp["dy"], inp["x"], inp["w"], inp["lam"], inp["u"], 0xF, out=outs)
+    torch.cuda.synchronize()
+    assert all(g.data_ptr() == o.data_ptr() for g, o in zip(got, outs))
+    check_grads(got, oracle_bwd(inp, 0xF), dtype, f"S={S} shift={shift}")
+
+
 def test_autograd_function_matches_oracle():
     wl = WORKLOADS["cls28_bf16_fb"].with_shape(B=1, C=8)
     inp = synth.make_inputs(wl, DEV)
