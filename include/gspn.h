@@ -149,6 +149,26 @@ int gspn_scan_fwd(const void* x, const void* w, const void* lam, const void* u, 
                   int64_t group_h, int64_t group_w, uint32_t flags, int algo,
                   void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * Forward scan that allocates nothing and takes no workspace, for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation).  Same arguments and result as
+ * gspn_scan_fwd with GSPN_ALGO_AUTO; the scratch memory the kernel families
+ * need comes from a fixed array of GSPN_NOALLOC_SCRATCH_BYTES inside the
+ * library, one per GPU, held until the process ends.
+ *   Returns GSPN_ERR_WORKSPACE, before anything runs, when the problem needs
+ *   more scratch than that (gspn_scan_fwd_workspace_bytes(..., AUTO) tells).
+ *   Every call on one GPU shares that GPU's array: calls that overlap in time
+ *   on one GPU (different streams, or host threads) race and must not be
+ *   issued.  Nothing in the array needs to start at zero; it keeps the last
+ *   call's contents.
+ */
+#define GSPN_NOALLOC_SCRATCH_BYTES (64u << 20)
+int gspn_scan_fwd_noalloc(const void* x, const void* w, const void* lam, const void* u, void* y,
+                          int64_t B, int64_t C, int64_t H, int64_t W, uint32_t mask,
+                          gspn_dtype dtype, int64_t group_h, int64_t group_w, uint32_t flags,
+                          void* stream);
+
 /* Bytes of workspace gspn_scan_bwd needs for this problem (0 if none).  With
  * GSPN_ALGO_AUTO the size covers every pointer alignment: AUTO runs the
  * streaming family, which needs a workspace, when a tensor the resident

@@ -5,6 +5,7 @@
 
 #include <algorithm>
 #include <cstdint>
+#include <mutex>
 #include <vector>
 
 #include "../../include/gspn.h"
@@ -12,7 +13,31 @@
 
 using namespace gspn;
 
+// Scratch of gspn_scan_fwd_noalloc: a file-scope device array, one copy per
+// GPU.  In host code `scratch` names a host-side stand-in, so host code uses
+// only the device address hipGetSymbolAddress returns (kept per device below).
+static __device__ __align__(256) unsigned char scratch[GSPN_NOALLOC_SCRATCH_BYTES];
+
 namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// device address of the current device's scratch array (looked up once per device)
+int scratch_for_current_device(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return GSPN_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return GSPN_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) return GSPN_ERR_HIP;
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return GSPN_OK;
+}
 
 constexpr size_t kWsAlign = 256;
 // families whose kernels take local-GSPN groups (the streaming family always does)
@@ -273,6 +298,26 @@ int gspn_scan_fwd(const void* x, const void* w, const void* lam, const void* u, 
   return GSPN_OK;
 }
 
+int gspn_scan_fwd_noalloc(const void* x, const void* w, const void* lam, const void* u, void* y,
+                          int64_t B, int64_t C, int64_t H, int64_t W, uint32_t mask, gspn_dtype dtype,
+                          int64_t group_h, int64_t group_w, uint32_t flags, void* stream) {
+  Problem p;
+  int st = check_shape(B, C, H, W, mask, dtype, group_h, group_w, flags, GSPN_ALGO_AUTO, &p);
+  if (st != GSPN_OK || p.empty) return st;
+  const int a = choose_algo(p, dtype, GSPN_ALGO_AUTO, false);
+  if (a < 0) return GSPN_ERR_UNSUPPORTED;
+  // the AUTO size also covers the streaming fallback of misaligned two-pass calls
+  const size_t need = fwd_ws_bytes(p, a, mask);
+  if (need > (size_t)GSPN_NOALLOC_SCRATCH_BYTES) return GSPN_ERR_WORKSPACE;
+  void* ws = nullptr;
+  if (need > 0) {
+    st = scratch_for_current_device(&ws);
+    if (st != GSPN_OK) return st;
+  }
+  return gspn_scan_fwd(x, w, lam, u, y, B, C, H, W, mask, dtype, group_h, group_w, flags, GSPN_ALGO_AUTO,
+                       ws, need > 0 ? (size_t)GSPN_NOALLOC_SCRATCH_BYTES : 0, stream);
+}
+
 int gspn_scan_bwd(const void* dy, const void* x, const void* w, const void* lam, const void* u,
                   void* dx, void* dw, void* dlam, void* du, int64_t B, int64_t C, int64_t H,
                   int64_t W, uint32_t mask, gspn_dtype dtype, int64_t group_h, int64_t group_w,
@@ -383,7 +428,8 @@ const char* gspn_strerror(int status) {
     case GSPN_ERR_ALIAS: return "an output overlaps an input or another output";
     case GSPN_ERR_UNSUPPORTED: return "unsupported: line longer than GSPN_MAX_LINE, too many planes, unknown flags, "
                                       "edge renormalisation without logits, negative group, or forced algorithm cannot run";
-    case GSPN_ERR_WORKSPACE: return "workspace missing or too small";
+    case GSPN_ERR_WORKSPACE: return "workspace missing or too small (gspn_scan_fwd_noalloc: the problem needs "
+                                    "more than GSPN_NOALLOC_SCRATCH_BYTES of scratch)";
     case GSPN_ERR_HIP: return "HIP runtime error";
     default: return "unknown status";
   }

@@ -24,8 +24,10 @@ STATUS = {0: "GSPN_OK", 1: "GSPN_ERR_NULL", 2: "GSPN_ERR_SHAPE", 3: "GSPN_ERR_MA
           7: "GSPN_ERR_UNSUPPORTED", 8: "GSPN_ERR_WORKSPACE", 9: "GSPN_ERR_HIP"}
 
 # every symbol include/gspn.h declares
-EXPORTS = ("gspn_scan_fwd_workspace_bytes", "gspn_scan_fwd", "gspn_scan_bwd_workspace_bytes",
-           "gspn_scan_bwd", "gspn_copy_calibration", "gspn_strerror", "gspn_version")
+EXPORTS = ("gspn_scan_fwd_workspace_bytes", "gspn_scan_fwd", "gspn_scan_fwd_noalloc",
+           "gspn_scan_bwd_workspace_bytes", "gspn_scan_bwd", "gspn_copy_calibration", "gspn_strerror",
+           "gspn_version")
+GSPN_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 _lib = None
 
@@ -55,6 +57,9 @@ def load() -> ctypes.CDLL:
     lib.gspn_scan_fwd.argtypes = [_p, _p, _p, _p, _p, _i64, _i64, _i64, _i64, _u32, _i, _i64, _i64, _u32,
                                   _i, _p, _sz, _p]
     lib.gspn_scan_fwd.restype = _i
+    lib.gspn_scan_fwd_noalloc.argtypes = [_p, _p, _p, _p, _p, _i64, _i64, _i64, _i64, _u32, _i, _i64, _i64,
+                                          _u32, _p]
+    lib.gspn_scan_fwd_noalloc.restype = _i
     lib.gspn_scan_bwd.argtypes = [_p, _p, _p, _p, _p, _p, _p, _p, _p, _i64, _i64, _i64, _i64, _u32,
                                   _i, _i64, _i64, _u32, _i, _p, _sz, _p]
     lib.gspn_scan_bwd.restype = _i
@@ -84,6 +89,12 @@ def gspn_scan_fwd(x, w, lam, u, y, B, C, H, W, mask, dtype, group_h, group_w, fl
                   workspace_bytes, stream) -> int:
     return int(load().gspn_scan_fwd(x, w, lam, u, y, B, C, H, W, mask, dtype, group_h, group_w, flags,
                                     algo, workspace, workspace_bytes, stream))
+
+
+def gspn_scan_fwd_noalloc(x, w, lam, u, y, B, C, H, W, mask, dtype, group_h, group_w, flags,
+                          stream) -> int:
+    return int(load().gspn_scan_fwd_noalloc(x, w, lam, u, y, B, C, H, W, mask, dtype, group_h, group_w,
+                                            flags, stream))
 
 
 def gspn_scan_bwd(dy, x, w, lam, u, dx, dw, dlam, du, B, C, H, W, mask, dtype, group_h, group_w, flags,
