@@ -41,8 +41,9 @@ int scratch_for_current_device(void** out) {
 
 constexpr size_t kWsAlign = 256;
 // families whose kernels take local-GSPN groups (the streaming family always does)
-constexpr bool kResidentGroups = false;
-constexpr bool kTwoPassGroups = false;
+constexpr bool kResidentGroupsFwd = true;
+constexpr bool kResidentGroupsBwd = true;
+constexpr bool kTwoPassGroups = true;
 
 size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
@@ -150,7 +151,7 @@ int check_ws(void* ws, size_t ws_bytes, size_t need,
 bool resident_fits(const Problem& p, int dtype, bool backward) {
   // the flags are implemented by the streaming family only; every family takes groups
   if (p.flags) return false;
-  if (p.grouped() && !kResidentGroups) return false;
+  if (p.grouped() && !(backward ? kResidentGroupsBwd : kResidentGroupsFwd)) return false;
   return gspn::resident_fits((int)p.H, (int)p.W, dtype, backward);
 }
 

@@ -116,6 +116,14 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
+// Local GSPN (groups of G lines along the scan axis): true when `line` is the
+// first line a scan visits in its group, where the state restarts from zero.
+// Forward scans enter a group [kG, (k+1)G) at its lowest line, reverse scans
+// at its highest one.  G = the line count (or more) is the global scan.
+__device__ __forceinline__ bool group_start(int line, int G, bool rev) {
+  return rev ? ((line + 1) % G == 0) : (line % G == 0);
+}
+
 // Calls f(std::integral_constant<int, i>) for i = B .. E-1 (compile-time indices,
 // fully unrolled by construction, where a large unrolled loop body may not be).
 template <int B, int E, typename F>

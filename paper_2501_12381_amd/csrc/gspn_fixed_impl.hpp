@@ -61,9 +61,11 @@ struct FixedCfg {
 // read).  After the middle barrier, and in phase H, lam * x and the
 // accumulator come from LDS, read G lines ahead of their use (never across the
 // middle barrier), so each input is read from HBM once.
-template <typename T, int S, bool HZ, bool REV, bool PRESENT>
+// GRP: local GSPN; bit l of gst is set when line l starts a group (the state
+// restarts from zero there).
+template <typename T, int S, bool HZ, bool REV, bool PRESENT, bool GRP>
 __device__ __forceinline__ void fixed_phase(const T* const (&pbase)[5], float* __restrict__ acc,
-                                            float* __restrict__ lxa, int sl) {
+                                            float* __restrict__ lxa, int sl, uint64_t gst) {
   using C = FixedCfg<T, S>;
   constexpr int TL = HZ ? C::THZ : 1;   // lines per tile
   constexpr int R = HZ ? C::RH : C::RV; // tiles in flight
@@ -145,6 +147,7 @@ __device__ __forceinline__ void fixed_phase(const T* const (&pbase)[5], float* _
         a = HZ ? ring[slot][2].get(e) : v1[2];
         b = HZ ? ring[slot][3].get(e) : v1[3];
         c = HZ ? ring[slot][4].get(e) : v1[4];
+        if (GRP && ((gst >> line_of(s)) & 1)) hp = 0.f;
         const float hl = from_prev_lane(hp), hr = from_next_lane(hp);
         float v = fmaf(a, hl, lx);
         v = fmaf(b, hp, v);
@@ -163,7 +166,7 @@ __device__ __forceinline__ void fixed_phase(const T* const (&pbase)[5], float* _
   }
 }
 
-template <typename T, int S>
+template <typename T, int S, bool GRP>
 __global__ void __launch_bounds__(128, (FixedCfg<T, S>::SEG < 64 ? 4 : 2))
 fixed_fwd_kernel(ResFwdParams p) {
   using C = FixedCfg<T, S>;
@@ -182,12 +185,13 @@ fixed_fwd_kernel(ResFwdParams p) {
     const int slot = p.slot[wave];
     const T* w0 = (const T*)p.w + (int64_t)(slot < 0 ? 0 : slot) * 3 * p.npc + plane * HW;
     const T* pb[5] = {(const T*)p.x + plane * HW, (const T*)p.lam + plane * HW, w0, w0 + p.npc, w0 + 2 * p.npc};
+    const uint64_t gst = p.gstart[wave][0];
     if (wave == 0) {
-      if (slot >= 0) fixed_phase<T, S, false, false, true>(pb, acc, lxa, sl);
-      else fixed_phase<T, S, false, false, false>(pb, acc, lxa, sl);
+      if (slot >= 0) fixed_phase<T, S, false, false, true, GRP>(pb, acc, lxa, sl, gst);
+      else fixed_phase<T, S, false, false, false, GRP>(pb, acc, lxa, sl, gst);
     } else {
-      if (slot >= 0) fixed_phase<T, S, false, true, true>(pb, acc, lxa, sl);
-      else fixed_phase<T, S, false, true, false>(pb, acc, lxa, sl);
+      if (slot >= 0) fixed_phase<T, S, false, true, true, GRP>(pb, acc, lxa, sl, gst);
+      else fixed_phase<T, S, false, true, false, GRP>(pb, acc, lxa, sl, gst);
     }
   }
   __syncthreads();
@@ -221,8 +225,9 @@ fixed_fwd_kernel(ResFwdParams p) {
       const T* w0 = (const T*)p.w + (int64_t)slot * 3 * p.npc + plane * HW;
       const T* pb[5] = {(const T*)p.x + plane * HW, (const T*)p.lam + plane * HW, w0, w0 + p.npc,
                         w0 + 2 * p.npc};
-      if (wave == 0) fixed_phase<T, S, true, false, true>(pb, acc, lxa, sl);
-      else fixed_phase<T, S, true, true, true>(pb, acc, lxa, sl);
+      const uint64_t gst = p.gstart[2 + wave][0];
+      if (wave == 0) fixed_phase<T, S, true, false, true, GRP>(pb, acc, lxa, sl, gst);
+      else fixed_phase<T, S, true, true, true, GRP>(pb, acc, lxa, sl, gst);
     }
   }
   __syncthreads();
@@ -275,7 +280,7 @@ inline bool fixed_size_supported(int H, int W) {
 template <typename T, int S>
 hipError_t launch_fixed(const ResFwdParams& p, hipStream_t st) {
   using C = FixedCfg<T, S>;
-  auto kern = fixed_fwd_kernel<T, S>;
+  auto kern = p.grouped ? fixed_fwd_kernel<T, S, true> : fixed_fwd_kernel<T, S, false>;
   if (C::LDS_BYTES > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
                                        C::LDS_BYTES);

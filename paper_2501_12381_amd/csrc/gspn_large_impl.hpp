@@ -63,6 +63,7 @@ struct LargeVParams {
   float* acc_b;      // split: the grid holds both directions as separate workgroups
                      // (blockIdx / planes), bottom-to-top writing its h here
   int split;
+  int grp;           // rows per local-GSPN group (H: the global scan)
 };
 
 // Layout of a row over a wave: the wave's span of 64 * NP positions is cut into
@@ -167,6 +168,14 @@ __global__ void __launch_bounds__(128 * WPD, 2) large_v_kernel(LargeVParams p) {
     const int t = t_of(s);
     const bool act = t >= 0 && t < H;
     const int par = s & 1;
+    // local GSPN: the first row of a group starts from a zero state (uniform per direction)
+    const bool rst = act && group_start(line_of(t), p.grp, dir != 0);
+    if (rst) {
+#pragma unroll
+      for (int q = 0; q < NQ; ++q)
+#pragma unroll
+        for (int j = 0; j < G; ++j) hp[q][j] = 0.f;
+    }
     // neighbours of each chunk's first and last position on the previous row
     float el[NQ], er[NQ];
 #pragma unroll
@@ -178,8 +187,8 @@ __global__ void __launch_bounds__(128 * WPD, 2) large_v_kernel(LargeVParams p) {
     if constexpr (WPD > 1) {
       const float nl = edge[par ^ 1][wi > 0 ? wave - 1 : wave][1];
       const float nr = edge[par ^ 1][wi < WPD - 1 ? wave + 1 : wave][0];
-      wl = wi > 0 ? nl : 0.f;
-      wr = wi < WPD - 1 ? nr : 0.f;
+      wl = (wi > 0 && !rst) ? nl : 0.f;
+      wr = (wi < WPD - 1 && !rst) ? nr : 0.f;
     }
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
@@ -316,6 +325,9 @@ struct LargeHParams {
   int band_rows, nbands, halo;
   int has_v;          // acc holds the vertical pass's partial sum
   const float* acc_b; // non-null: the vertical sum is acc + acc_b until the first horizontal direction adds
+  // local GSPN, per direction (left-to-right, right-to-left): bit i set when
+  // window column i of this launch starts a group (the state restarts from zero)
+  uint64_t gmask[2];
 };
 
 template <typename T, int NW>
@@ -405,6 +417,7 @@ __global__ void __launch_bounds__(64 * NW) large_h_kernel(LargeHParams p) {
     }
   };
 
+  const uint64_t gm = p.gmask[dir];
   auto scan = [&](auto rev_tag) __attribute__((always_inline)) {
     constexpr bool REV = decltype(rev_tag)::value;
     // the tile is loaded map by map, each row segment's vectors back to back:
@@ -428,12 +441,14 @@ __global__ void __launch_bounds__(64 * NW) large_h_kernel(LargeHParams p) {
       const int ti = REV ? K - 1 - i : i;  // window column of this step
       if (ti < lo) return;                 // short last block (uniform)
       const int par = i & 1;
+      const bool rst = (gm >> ti) & 1;  // this column starts a group (uniform)
+      if (rst) hp = 0.f;
       float up = from_prev_lane(hp), dn = from_next_lane(hp);
       if constexpr (NW > 1) {
         const float nu = edge[((par ^ 1) * NW + (wave > 0 ? wave - 1 : wave)) * 2 + 1];
         const float nd = edge[((par ^ 1) * NW + (wave < NW - 1 ? wave + 1 : wave)) * 2 + 0];
-        if (lane == 0) up = wave > 0 ? nu : 0.f;
-        if (lane == 63) dn = wave < NW - 1 ? nd : 0.f;
+        if (lane == 0) up = (wave > 0 && !rst) ? nu : 0.f;
+        if (lane == 63) dn = (wave < NW - 1 && !rst) ? nd : 0.f;
       }
       const float xv = tile[0][ti / VE].get(ti % VE), lv = tile[1][ti / VE].get(ti % VE);
       const float a = tile[2][ti / VE].get(ti % VE), bw = tile[3][ti / VE].get(ti % VE),
@@ -598,6 +613,7 @@ hipError_t large_fwd_t(const LargeFwdArgs& a) {
     // both vertical directions feeding a horizontal pass: twice the workgroups,
     // one direction each, each with its own partial sum (no midpoint pairing,
     // so the grid has no partly filled last round of whole planes)
+    v.grp = (a.group_h > 0 && a.group_h < a.H) ? a.group_h : a.H;
     v.split = slot[0] >= 0 && slot[1] >= 0 && has_h && a.acc_b != nullptr;
     v.acc_b = a.acc_b;
     if (v.split && 2 * a.planes > 0x7fffffffLL) return hipErrorInvalidConfiguration;
@@ -625,8 +641,25 @@ hipError_t large_fwd_t(const LargeFwdArgs& a) {
   h.acc_b = (slot[0] >= 0 && slot[1] >= 0 && a.acc_b != nullptr) ? a.acc_b : nullptr;
   const int64_t grid = (int64_t)g.nbands * a.planes * (both ? 2 : 1);
   if (grid > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+  const int GW = (a.group_w > 0 && a.group_w < a.W) ? a.group_w : a.W;
+  // bit i of the mask: window column i of the launch starts a group
+  auto window_mask = [&](int dir, int seq) -> uint64_t {
+    if (seq < 0 || seq >= g.nblk || GW >= a.W) return 0;
+    const int blk = dir ? g.nblk - 1 - seq : seq;
+    const int c0 = blk * C::KH;
+    const int ws = c0 + C::KH <= a.W ? c0 : a.W - C::KH;
+    uint64_t m = 0;
+    for (int i = 0; i < C::KH; ++i) {
+      const int c = ws + i;
+      if (dir ? ((c + 1) % GW == 0) : (c % GW == 0)) m |= 1ull << i;
+    }
+    return m;
+  };
+  static_assert(C::KH <= 64, "one mask bit per window column");
   for (int j = 0; j < g.nblk + h.delay; ++j) {
     h.step = j;
+    h.gmask[0] = window_mask(0, j);
+    h.gmask[1] = window_mask(1, j - h.delay);
     hipError_t e = launch_large_h<T>(h, g.nw, grid, g.lds_h, st);
     if (e != hipSuccess) return e;
   }

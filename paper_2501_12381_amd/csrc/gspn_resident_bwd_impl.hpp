@@ -62,6 +62,10 @@ struct ResBwdParams {
   int slot[4];
   int nd;   // directions present
   int vec;  // 16-byte vectors legal for the elementwise passes
+  int grouped;          // local GSPN: some direction restarts inside the plane
+  // per direction (T2B, B2T, L2R, R2L): bit l set when line l starts a group
+  // in that direction's scan order (lines <= 64)
+  uint64_t gstart[4];
 };
 
 // Input ring shared by phase F (x, lam, w0, w1, w2) and phase A (u, dy, w0, w1, w2).
@@ -85,7 +89,8 @@ struct Ring {
 
 // Forward recompute of one direction into its LDS array: h[line][pos].
 template <typename T, int S, bool HZ, bool REV>
-__device__ __forceinline__ void bwd_forward(const T* const (&pb)[5], float* __restrict__ harr, int sl) {
+__device__ __forceinline__ void bwd_forward(const T* const (&pb)[5], float* __restrict__ harr, int sl,
+                                            uint64_t gst) {
   using C = BwdCfg<T, S>;
   using RG = Ring<T, S, HZ, REV>;
   constexpr int TL = RG::TL, R = RG::R, NT = RG::NT;
@@ -112,6 +117,7 @@ __device__ __forceinline__ void bwd_forward(const T* const (&pb)[5], float* __re
       const int e = REV ? TL - 1 - ee : ee;
       const int line = RG::tile_line(ti) + e;
       float xv[1] = {v[0][e]}, lv[1] = {v[1][e]}, a[1] = {v[2][e]}, b[1] = {v[3][e]}, c[1] = {v[4][e]};
+      if ((gst >> line) & 1) hp[0] = 0.f;  // local GSPN: a group starts here
       line_step<1>(xv, lv, a, b, c, vv, hp);
       harr[aoff + (HZ ? line : line * C::P)] = hp[0];
     }
@@ -122,7 +128,7 @@ __device__ __forceinline__ void bwd_forward(const T* const (&pb)[5], float* __re
 // writes the direction's three dw maps.
 template <typename T, int S, bool HZ, bool REV>
 __device__ __forceinline__ void bwd_adjoint(const T* const (&pb)[5], T* const (&dwp)[3],
-                                            float* __restrict__ harr, int sl) {
+                                            float* __restrict__ harr, int sl, uint64_t gst) {
   using C = BwdCfg<T, S>;
   // the adjoint visits lines in the opposite order of the forward scan
   using RG = Ring<T, S, HZ, !REV>;
@@ -153,7 +159,11 @@ __device__ __forceinline__ void bwd_adjoint(const T* const (&pb)[5], T* const (&
       const int line = RG::tile_line(ti) + e;
       // previous line in forward order (its h is the state this line read)
       const int prev = REV ? line + 1 : line - 1;
-      const bool has_prev = REV ? line + 1 < S : line > 0;
+      // a line that starts a group read a zero state, and the line after it in
+      // forward order, if it starts a group, took nothing from this one
+      const bool has_prev = (REV ? line + 1 < S : line > 0) && !((gst >> line) & 1);
+      const int succ = REV ? line - 1 : line + 1;
+      if (succ >= 0 && succ < S && ((gst >> succ) & 1)) gn = 0.f;
       const float a0 = wn0 * gn, a1 = wn1 * gn, a2 = wn2 * gn;
       const float a0n = from_next_lane(a0);  // neighbour p+1 received with k = 0
       const float a2p = from_prev_lane(a2);  // neighbour p-1 received with k = 2
@@ -239,10 +249,10 @@ __global__ void __launch_bounds__(256, 2) resident_bwd_kernel(ResBwdParams p) {
   if (slot >= 0) {
     const T* pb[5] = {(const T*)p.x + pofs, (const T*)p.lam + pofs, w0, w0 + p.npc, w0 + 2 * p.npc};
     switch (wave) {
-      case 0: bwd_forward<T, S, false, false>(pb, harr, sl); break;
-      case 1: bwd_forward<T, S, false, true>(pb, harr, sl); break;
-      case 2: bwd_forward<T, S, true, false>(pb, harr, sl); break;
-      default: bwd_forward<T, S, true, true>(pb, harr, sl); break;
+      case 0: bwd_forward<T, S, false, false>(pb, harr, sl, p.gstart[0]); break;
+      case 1: bwd_forward<T, S, false, true>(pb, harr, sl, p.gstart[1]); break;
+      case 2: bwd_forward<T, S, true, false>(pb, harr, sl, p.gstart[2]); break;
+      default: bwd_forward<T, S, true, true>(pb, harr, sl, p.gstart[3]); break;
     }
   }
   __syncthreads();
@@ -264,10 +274,10 @@ __global__ void __launch_bounds__(256, 2) resident_bwd_kernel(ResBwdParams p) {
     T* dw0 = (T*)p.dw + (int64_t)slot * 3 * p.npc + pofs;
     T* const dwp[3] = {dw0, dw0 + p.npc, dw0 + 2 * p.npc};
     switch (wave) {
-      case 0: bwd_adjoint<T, S, false, false>(pb, dwp, harr, sl); break;
-      case 1: bwd_adjoint<T, S, false, true>(pb, dwp, harr, sl); break;
-      case 2: bwd_adjoint<T, S, true, false>(pb, dwp, harr, sl); break;
-      default: bwd_adjoint<T, S, true, true>(pb, dwp, harr, sl); break;
+      case 0: bwd_adjoint<T, S, false, false>(pb, dwp, harr, sl, p.gstart[0]); break;
+      case 1: bwd_adjoint<T, S, false, true>(pb, dwp, harr, sl, p.gstart[1]); break;
+      case 2: bwd_adjoint<T, S, true, false>(pb, dwp, harr, sl, p.gstart[2]); break;
+      default: bwd_adjoint<T, S, true, true>(pb, dwp, harr, sl, p.gstart[3]); break;
     }
   }
   // an absent direction's array stays zero from the initial fill

@@ -89,6 +89,7 @@ struct Phase {
   int Pn;  // positions per line
   int W;   // row pitch of the global tensors
   int P;   // row pitch of the LDS accumulator
+  int G;   // lines per local-GSPN group (L: the global scan)
 };
 
 // The five inputs of a line step: x, lam, w0, w1, w2 (pointers at the plane base).
@@ -230,8 +231,12 @@ __device__ __forceinline__ void scan_v(const Maps<T>& mp, const Phase& g, float*
 #pragma unroll
           for (int q = 0; q < NP; ++q) v[m][q] = ring[k][m].get(q);
         load_slot(ring[k], s + D);
-        line_step<NP>(v[0], v[1], v[2], v[3], v[4], valid, hp);
         const int line = line_of(s);
+        if (group_start(line, g.G, REV)) {
+#pragma unroll
+          for (int q = 0; q < NP; ++q) hp[q] = 0.f;
+        }
+        line_step<NP>(v[0], v[1], v[2], v[3], v[4], valid, hp);
         int off[NP], noff[NP];
 #pragma unroll
         for (int q = 0; q < NP; ++q) {
@@ -296,6 +301,10 @@ __device__ __forceinline__ void scan_h(const Maps<T>& mp, const Phase& g, float*
         for (int m = 0; m < 5; ++m)
 #pragma unroll
           for (int q = 0; q < NP; ++q) v[m][q] = tl[m][q][l / VL].get(l % VL);
+        if (group_start(line, g.G, REV)) {
+#pragma unroll
+          for (int q = 0; q < NP; ++q) hp[q] = 0.f;
+        }
         line_step<NP>(v[0], v[1], v[2], v[3], v[4], valid, hp);
         int off[NP], noff[NP];
 #pragma unroll
@@ -374,6 +383,11 @@ struct ResFwdParams {
   int H, W, P;  // P: LDS row pitch (odd, > W)
   int slot[4];  // T2B, B2T, L2R, R2L -> weight slot or -1
   int vec_y;
+  int gh, gw;   // local-GSPN group lengths along rows and columns (the line count: global)
+  int grouped;  // gh < H or gw < W
+  // per direction (T2B, B2T, L2R, R2L): bit l of word l / 64 set when line l
+  // (< 128) starts a group in that direction's scan order
+  uint64_t gstart[4][2];
 };
 
 template <typename T, int NP, int SEG, int DV, int PDH, bool VV, int VL, int MINW>
@@ -404,6 +418,7 @@ __global__ void __launch_bounds__(128, MINW) resident_fwd_kernel(ResFwdParams p)
     g.Pn = hz ? p.H : p.W;
     g.W = p.W;
     g.P = p.P;
+    g.G = hz ? p.gw : p.gh;
     if (slot < 0) {
       // the direction is not in the mask: keep the phase's barriers in step
       const int nbar = (g.L & 1) ? 2 : 1;
@@ -527,13 +542,23 @@ hipError_t resident_fwd_t(const ResidentFwdArgs& a) {
   p.H = a.H; p.W = a.W; p.P = c.P;
   int n = 0;
   for (int d = 0; d < 4; ++d) p.slot[d] = (a.mask >> d) & 1 ? n++ : -1;
+  p.gh = (a.group_h > 0 && a.group_h < a.H) ? a.group_h : a.H;
+  p.gw = (a.group_w > 0 && a.group_w < a.W) ? a.group_w : a.W;
+  p.grouped = p.gh < a.H || p.gw < a.W;
+  for (int d = 0; d < 4; ++d) {
+    const bool hz = d >= 2, rev = d & 1;
+    const int L = hz ? a.W : a.H, G = hz ? p.gw : p.gh;
+    p.gstart[d][0] = p.gstart[d][1] = 0;
+    for (int l = 0; l < L && l < 128; ++l)
+      if (rev ? ((l + 1) % G == 0 || l == L - 1) : (l % G == 0)) p.gstart[d][l >> 6] |= 1ull << (l & 63);
+  }
   // epilogue vectors: 16 bytes if rows allow, else 8 bytes, else scalars
   const int v16 = 16 / (int)sizeof(T), v8 = 8 / (int)sizeof(T);
   p.vec_y = (a.W % v16 == 0 && al(a.u, 16) && al(a.y, 16)) ? 2
           : (a.W % v8 == 0 && al(a.u, 8) && al(a.y, 8)) ? 1 : 0;
   hipStream_t st = (hipStream_t)a.stream;
-  if (a.use_fixed && a.H == 128 && a.W == 128 && al(a.x, 16) && al(a.lam, 16) && al(a.w, 16) && al(a.u, 16) &&
-      al(a.y, 16))
+  if (a.use_fixed && !p.grouped && a.H == 128 && a.W == 128 && al(a.x, 16) && al(a.lam, 16) && al(a.w, 16) &&
+      al(a.u, 16) && al(a.y, 16))
     return launch_wide<T>(p, st);  // persistent, every input read once
   if (a.use_fixed && fixed_size_supported(a.H, a.W) && al(a.x, 16) && al(a.lam, 16) && al(a.w, 16)) {
     switch (a.H) {

@@ -77,9 +77,10 @@ __device__ __forceinline__ void lds_put2(float* p, float a, float b) { *reinterp
 
 // One direction's forward recompute from LDS into harr.  harr holds lam * x on
 // entry; each line's entry is read (one pair ahead) before h overwrites it.
-template <typename T, int S, bool HZ, bool REV>
+// GRP: local GSPN; bit l of gst is set when line l starts a group.
+template <typename T, int S, bool HZ, bool REV, bool GRP>
 __device__ __forceinline__ void staged_forward(const T* __restrict__ w3, float* __restrict__ harr, int sl,
-                                               bool lane_ok) {
+                                               bool lane_ok, uint64_t gst) {
   using C = StagedCfg<T, S>;
   constexpr int NP = S / 2;
   const bool valid = lane_ok && sl < S;
@@ -125,6 +126,7 @@ __device__ __forceinline__ void staged_forward(const T* __restrict__ w3, float* 
     float hv[2];
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
+      if (GRP && ((gst >> line_of(2 * j + t)) & 1)) hp = 0.f;  // a group starts at this line
       const float hl = from_prev_lane(hp), hr = from_next_lane(hp);
       float h = fmaf(cur[t][2], hp, cur[t][0]);
       h = fmaf(cur[t][1], hl, h);
@@ -145,9 +147,10 @@ __device__ __forceinline__ void staged_forward(const T* __restrict__ w3, float* 
 // g overwrites h.  Padding lanes (and lanes of absent planes) hold g = 0, so
 // their finite weights (absent planes' are zero-filled) send nothing to a
 // real lane; their stores are skipped.
-template <typename T, int S, bool HZ, bool REV>
+template <typename T, int S, bool HZ, bool REV, bool GRP>
 __device__ __forceinline__ void staged_adjoint(const float* __restrict__ udy, T* __restrict__ w3,
-                                               float* __restrict__ harr, int sl, bool lane_ok) {
+                                               float* __restrict__ harr, int sl, bool lane_ok,
+                                               uint64_t gst) {
   using C = StagedCfg<T, S>;
   constexpr int NP = S / 2;
   const bool valid = lane_ok && sl < S;
@@ -155,7 +158,8 @@ __device__ __forceinline__ void staged_adjoint(const float* __restrict__ udy, T*
   const int aoff = valid ? (HZ ? sl * C::P : sl) : (HZ ? S * C::P : S);
   auto line_of = [](int s) { return REV ? s : S - 1 - s; };  // against the scan order
   auto prev_of = [](int line) { return REV ? line + 1 : line - 1; };  // previous line in scan order
-  auto has_prev = [](int line) { return REV ? line + 1 < S : line > 0; };
+  // a line that starts a group read a zero state
+  auto has_prev = [&](int line) { return (REV ? line + 1 < S : line > 0) && !(GRP && ((gst >> line) & 1)); };
   auto elem = [&](int line) { return HZ ? pos * S + line : line * S + pos; };
   auto aidx = [&](int line) { return aoff + (HZ ? line : line * C::P); };
   auto pair_lo = [](int j) { return REV ? 2 * j : S - 2 - 2 * j; };
@@ -197,7 +201,11 @@ __device__ __forceinline__ void staged_adjoint(const float* __restrict__ udy, T*
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
       // u * dy + transposed stencil of the next line (neighbour p+1 sends its
-      // k = 0 term, neighbour p-1 its k = 2 term)
+      // k = 0 term, neighbour p-1 its k = 2 term); none when that line starts a group
+      if constexpr (GRP) {
+        const int succ = REV ? line_of(2 * j + t) - 1 : line_of(2 * j + t) + 1;
+        if (succ >= 0 && succ < S && ((gst >> succ) & 1)) gn = 0.f;
+      }
       const float a0 = wn0 * gn, a2 = wn2 * gn;
       float g = fmaf(wn1, gn, cur[t][0]);
       g += from_next_lane(a0);
@@ -243,7 +251,7 @@ __device__ __forceinline__ int staged_aidx(int e0, int r0, int c0, int q) {
 // ND: directions present (compile time, so every index below divides by
 // constants).  Direction arrays are indexed by slot (present directions in
 // increasing direction order), [plane][slot][(S + 1) x (S + 1)].
-template <typename T, int S, int ND>
+template <typename T, int S, int ND, bool GRP>
 __global__ void __launch_bounds__(256) staged_bwd_kernel(ResBwdParams p) {
   using C = StagedCfg<T, S>;
   constexpr int PPW = C::PPW, HW = C::HW, NVM = C::NVM, VE = C::VE, MV = C::MV;
@@ -333,10 +341,10 @@ __global__ void __launch_bounds__(256) staged_bwd_kernel(ResBwdParams p) {
 
   if (slot >= 0) {
     switch (wave) {
-      case 0: staged_forward<T, S, false, false>(w3, harr, sl, lane_ok); break;
-      case 1: staged_forward<T, S, false, true>(w3, harr, sl, lane_ok); break;
-      case 2: staged_forward<T, S, true, false>(w3, harr, sl, lane_ok); break;
-      default: staged_forward<T, S, true, true>(w3, harr, sl, lane_ok); break;
+      case 0: staged_forward<T, S, false, false, GRP>(w3, harr, sl, lane_ok, p.gstart[0]); break;
+      case 1: staged_forward<T, S, false, true, GRP>(w3, harr, sl, lane_ok, p.gstart[1]); break;
+      case 2: staged_forward<T, S, true, false, GRP>(w3, harr, sl, lane_ok, p.gstart[2]); break;
+      default: staged_forward<T, S, true, true, GRP>(w3, harr, sl, lane_ok, p.gstart[3]); break;
     }
   }
   lds_barrier();
@@ -370,10 +378,10 @@ __global__ void __launch_bounds__(256) staged_bwd_kernel(ResBwdParams p) {
 
   if (slot >= 0) {
     switch (wave) {
-      case 0: staged_adjoint<T, S, false, false>(s_udy + sg * HW, w3, harr, sl, lane_ok); break;
-      case 1: staged_adjoint<T, S, false, true>(s_udy + sg * HW, w3, harr, sl, lane_ok); break;
-      case 2: staged_adjoint<T, S, true, false>(s_udy + sg * HW, w3, harr, sl, lane_ok); break;
-      default: staged_adjoint<T, S, true, true>(s_udy + sg * HW, w3, harr, sl, lane_ok); break;
+      case 0: staged_adjoint<T, S, false, false, GRP>(s_udy + sg * HW, w3, harr, sl, lane_ok, p.gstart[0]); break;
+      case 1: staged_adjoint<T, S, false, true, GRP>(s_udy + sg * HW, w3, harr, sl, lane_ok, p.gstart[1]); break;
+      case 2: staged_adjoint<T, S, true, false, GRP>(s_udy + sg * HW, w3, harr, sl, lane_ok, p.gstart[2]); break;
+      default: staged_adjoint<T, S, true, true, GRP>(s_udy + sg * HW, w3, harr, sl, lane_ok, p.gstart[3]); break;
     }
   }
   lds_barrier();
@@ -437,7 +445,7 @@ template <typename T, int S, int ND>
 hipError_t launch_staged_bwd_nd(const ResBwdParams& p, hipStream_t st) {
   using C = StagedCfg<T, S>;
   constexpr int lds = C::bytes(C::PPW, ND);
-  auto kern = staged_bwd_kernel<T, S, ND>;
+  auto kern = p.grouped ? staged_bwd_kernel<T, S, ND, true> : staged_bwd_kernel<T, S, ND, false>;
   if (lds > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     if (e != hipSuccess) return e;
@@ -478,6 +486,16 @@ hipError_t resident_bwd_t(const ResidentBwdArgs& a) {
   int n = 0;
   for (int d = 0; d < 4; ++d) p.slot[d] = (a.mask >> d) & 1 ? n++ : -1;
   p.nd = n;
+  const int gh = (a.group_h > 0 && a.group_h < a.H) ? a.group_h : a.H;
+  const int gw = (a.group_w > 0 && a.group_w < a.W) ? a.group_w : a.W;
+  p.grouped = gh < a.H || gw < a.W;
+  for (int d = 0; d < 4; ++d) {
+    const bool hz = d >= 2, rev = d & 1;
+    const int L = hz ? a.W : a.H, G = hz ? gw : gh;
+    p.gstart[d] = 0;
+    for (int l = 0; l < L && l < 64; ++l)
+      if (rev ? ((l + 1) % G == 0 || l == L - 1) : (l % G == 0)) p.gstart[d] |= 1ull << l;
+  }
   auto al16 = [](const void* q) { return ((uintptr_t)q % 16) == 0; };
   p.vec = al16(a.dy) && al16(a.x) && al16(a.lam) && al16(a.u) && al16(a.dx) && al16(a.dlam) && al16(a.du);
   const bool ok = al16(a.x) && al16(a.lam) && al16(a.w) && al16(a.u) && al16(a.dy) && al16(a.dw);

@@ -118,13 +118,6 @@ struct Edges {
   float hi[2][kMaxWaves];  // [parity][wave] value at the wave's last position
 };
 
-// Lines per group and the group-start test (local GSPN): a forward scan
-// enters a group [kG, (k+1)G) at its lowest line, a reverse scan at its
-// highest one; the state is reset to zero there.
-__device__ __forceinline__ bool group_start(int line, int G, bool rev) {
-  return rev ? ((line + 1) % G == 0) : (line % G == 0);
-}
-
 // Eq. 6: the three logits of one pixel -> its three weights (sigmoid, then
 // normalised over the neighbours that count: all three, or with edge
 // renormalisation the ones on the line).  Also returns the sigmoids and the

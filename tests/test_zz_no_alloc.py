@@ -54,7 +54,7 @@ CASES = [
     ((1, 3, 300, 256, 0xF, torch.bfloat16, 0), (1, 1, 300, 64, 0xF, torch.bfloat16, 0)),
     ((1, 2, 520, 1032, 0xF, torch.bfloat16, 0), (1, 1, 400, 64, 0x7, torch.bfloat16, 0)),
     ((2, 2, 90, 2049, 0xF, torch.float32, 0), (1, 1, 33, 2049, 0xB, torch.float32, 0)),
-    ((1, 2, 300, 256, 0xF, torch.float32, 40), (1, 1, 100, 200, 0xF, torch.float32, 7)),
+    ((1, 2, 300, 256, 0xF, torch.float32, 40), (1, 1, 100, 2049, 0xF, torch.float32, 7)),
 ]
 
 
