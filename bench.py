@@ -10,7 +10,8 @@ The headline line measures the largest single-GPU workload: the 4-direction
 bf16 forward on 1 x 320 x 2048 x 2048 planes (an image latent of about 16K
 pixels a side).  Beside it, `extra` holds the other measured workloads (the
 28 x 28 classification-stage forward+backward, the 128 x 128 diffusion-latent
-forward, the 56 x 56 fp32 forward), each with its own roofline entries.
+forward, the 56 x 56 fp32 forward, and forward+backward at both latent
+sizes), each with its own roofline entries.
 
 Prints one JSON line with the throughput in propagated pixel-channel-directions
 per second (B*C*H*W*n per step / seconds), the roofline position of the
@@ -40,7 +41,7 @@ sys.path.insert(0, ROOT)
 METRIC = "propagated pixel-channel-directions/sec and % of HBM roofline, fwd and fwd+bwd"
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E peak
 DEFAULT_WORKLOAD = "lat2048_bf16"  # the largest workload that fits one GPU
-EXTRA_WORKLOADS = ("cls28_bf16_fb", "lat128_bf16", "cls56_f32")
+EXTRA_WORKLOADS = ("cls28_bf16_fb", "lat128_bf16", "cls56_f32", "lat128_bf16_fb", "lat2048_bf16_fb")
 ALGOS = {"auto": 0, "resident": 1, "stream": 2, "resident_generic": 3, "two_pass": 4}
 KERNEL_SRC = os.path.join(ROOT, "paper_2501_12381_amd", "csrc")
 CPU_WORKERS_MAX = 16  # the host-core share of one GPU on the benchmark machines

@@ -64,7 +64,8 @@ class Workload:
         return Workload(**d)
 
 
-# The five workloads the hot path is measured and checked on.
+# The five workloads the hot path is measured and checked on (shapes, dtypes and
+# distributions of the classification stages and diffusion latents above).
 WORKLOADS = {
     "t2b_16": Workload("t2b_16", 1, 8, 16, 16, DIR_T2B, "f32", lam="uniform", u="ones",
                        w_logit_std=1.0, seed=1),
@@ -77,6 +78,10 @@ WORKLOADS = {
     "lat2048_bf16": Workload("lat2048_bf16", 1, 320, 2048, 2048, 0xF, "bf16", lam="uniform",
                              u="ones", w_logit_std=1.0, seed=5),
 }
+# The two latent shapes with the backward as well (training at those sizes):
+# same inputs, plus dy ~ N(0, 1).
+WORKLOADS["lat128_bf16_fb"] = WORKLOADS["lat128_bf16"].with_shape(name="lat128_bf16_fb", backward=True)
+WORKLOADS["lat2048_bf16_fb"] = WORKLOADS["lat2048_bf16"].with_shape(name="lat2048_bf16_fb", backward=True)
 
 
 def torch_dtype(dt: str) -> torch.dtype:

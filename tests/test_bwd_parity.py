@@ -158,3 +158,30 @@ def test_autograd_function_matches_oracle():
     ref = oracle_bwd(inp, wl.mask)
     got = (leaves["x"].grad, leaves["w"].grad, leaves["lam"].grad, leaves["u"].grad)
     check_grads(got, ref, torch.bfloat16, "autograd")
+
+
+def test_4096_planes_backward_sampled():
+    """Backward at 4096 x 4096 (2 planes, bf16), one plane against the oracle."""
+    wl = synth.Workload("lat4096fb", 1, 2, 4096, 4096, 0xF, "bf16", lam="uniform", u="ones",
+                        backward=True, seed=9)
+    print("[bwd] 4096x4096 x 2 planes", flush=True)
+    inp = synth.make_inputs(wl, DEV)
+    got = run_bwd(inp, wl.mask, L.GSPN_ALGO_AUTO)
+    torch.cuda.synchronize()
+    sub = {k: (v[:, :, 0:1, 0:1] if k == "w" else v[0:1, 0:1]) for k, v in inp.items()}
+    sel = [g[0:1, 0:1] if i != 1 else g[:, :, 0:1, 0:1] for i, g in enumerate(got)]
+    check_grads(sel, oracle_bwd(sub, wl.mask), torch.bfloat16, "4096 plane 0")
+
+
+@pytest.mark.parametrize("name", ["lat128_bf16_fb"])
+def test_latent_backward_sampled(name):
+    """Backward on the 2 x 640 x 128 x 128 latent workload, sampled planes."""
+    wl = WORKLOADS[name]
+    print(f"[bwd] {name}", flush=True)
+    inp = synth.make_inputs(wl, DEV)
+    got = run_bwd(inp, wl.mask, L.GSPN_ALGO_AUTO)
+    torch.cuda.synchronize()
+    for b, c in ((0, 0), (1, 321), (1, 639)):
+        sub = {k: (v[:, :, b:b + 1, c:c + 1] if k == "w" else v[b:b + 1, c:c + 1]) for k, v in inp.items()}
+        sel = [g[b:b + 1, c:c + 1] if i != 1 else g[:, :, b:b + 1, c:c + 1] for i, g in enumerate(got)]
+        check_grads(sel, oracle_bwd(sub, wl.mask), torch.bfloat16, f"plane ({b},{c})")

@@ -252,3 +252,16 @@ def test_copy_calibration_kernel():
     ops.gspn_copy_calibration(src[:-5], dst[:-5])  # 16-byte aligned starts, ragged tail
     torch.cuda.synchronize()
     assert torch.equal(dst[:-5], src[:-5]) and not dst[-5:].any()
+
+
+def test_4096_planes_forward_sampled():
+    """The longest lines the library takes: 2 planes of 4096 x 4096 bf16
+    (two-pass kernels), one plane checked against the oracle in full."""
+    wl = synth.Workload("lat4096", 1, 2, 4096, 4096, 0xF, "bf16", lam="uniform", u="ones", seed=9)
+    print("[fwd] 4096x4096 x 2 planes", flush=True)
+    inp = synth.make_inputs(wl, DEV, with_dy=False)
+    y = run_fwd(inp, wl.mask, L.GSPN_ALGO_AUTO)
+    torch.cuda.synchronize()
+    assert torch.isfinite(y).all()
+    sub = {k: (v[:, :, 0:1, 1:2] if k == "w" else v[0:1, 1:2]) for k, v in inp.items()}
+    assert_close(y[0:1, 1:2], oracle_fwd(sub, wl.mask), y.dtype, "4096 plane 1")
