@@ -298,7 +298,7 @@ __global__ void __launch_bounds__(256, 2) resident_bwd_kernel(ResBwdParams p) {
 }
 
 inline bool resident_bwd_size_supported(int H, int W) {
-  return H == W && (H == 16 || H == 28 || H == 32 || H == 56 || H == 64);
+  return H == W && (H == 16 || H == 28 || H == 32 || H == 56 || H == 64 || H == 128);
 }
 
 template <typename T, int S>

@@ -22,6 +22,7 @@
 #include "gspn_launch.hpp"
 #include "gspn_resident_impl.hpp"
 #include "gspn_resident_bwd_impl.hpp"
+#include "gspn_widebwd_impl.hpp"
 
 namespace gspn {
 
@@ -501,6 +502,25 @@ hipError_t resident_bwd_t(const ResidentBwdArgs& a) {
   const bool ok = al16(a.x) && al16(a.lam) && al16(a.w) && al16(a.u) && al16(a.dy) && al16(a.dw);
   if (!ok || !resident_bwd_size_supported(a.H, a.W)) return hipErrorInvalidValue;
   hipStream_t st = (hipStream_t)a.stream;
+  if (a.H == 128) {
+    // persistent 128 x 128 kernel: every pointer 16-byte aligned
+    if (!p.vec) return hipErrorInvalidValue;
+    WideBwdParams q;
+    q.dy = a.dy; q.x = a.x; q.lam = a.lam; q.w = a.w; q.u = a.u;
+    q.dx = a.dx; q.dw = a.dw; q.dlam = a.dlam; q.du = a.du;
+    q.npc = p.npc; q.planes = a.planes;
+    for (int d = 0; d < 4; ++d) q.slot[d] = p.slot[d];
+    const int gh = (a.group_h > 0 && a.group_h < 128) ? a.group_h : 128;
+    const int gw = (a.group_w > 0 && a.group_w < 128) ? a.group_w : 128;
+    for (int d = 0; d < 4; ++d) {
+      const bool rev = d & 1;
+      const int G = d >= 2 ? gw : gh;
+      q.gstart[d][0] = q.gstart[d][1] = 0;
+      for (int l = 0; l < 128; ++l)
+        if (rev ? ((l + 1) % G == 0 || l == 127) : (l % G == 0)) q.gstart[d][l >> 6] |= 1ull << (l & 63);
+    }
+    return sizeof(T) == 4 ? wide_bwd_launch_f32(q, st) : wide_bwd_launch_bf16(q, st);
+  }
   if (a.use_staged && p.vec && staged_bwd_size_supported<T>(a.H, a.W))
     return launch_staged_bwd_size<T>(p, a.H, st);
   switch (a.H) {

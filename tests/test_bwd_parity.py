@@ -185,3 +185,37 @@ def test_latent_backward_sampled(name):
         sub = {k: (v[:, :, b:b + 1, c:c + 1] if k == "w" else v[b:b + 1, c:c + 1]) for k, v in inp.items()}
         sel = [g[b:b + 1, c:c + 1] if i != 1 else g[:, :, b:b + 1, c:c + 1] for i, g in enumerate(got)]
         check_grads(sel, oracle_bwd(sub, wl.mask), torch.bfloat16, f"plane ({b},{c})")
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16], ids=["f32", "bf16"])
+@pytest.mark.parametrize("mask", [1, 2, 4, 8, 3, 12, 5, 10, 7, 14, 15])
+def test_bwd_128_every_direction_set(mask, dtype):
+    """128 x 128 planes (the persistent backward kernel): direction subsets,
+    through AUTO and the forced resident family."""
+    print(f"[bwd] 128x128 mask {mask} {dtype}", flush=True)
+    t = synth.random_general((1, 3, 128, 128), ops.n_dirs(mask), device=DEV, seed=500 + mask)
+    t = {k: v.to(dtype) for k, v in t.items()}
+    ref = oracle_bwd(t, mask)
+    for algo in (L.GSPN_ALGO_AUTO, L.GSPN_ALGO_RESIDENT):
+        got = run_bwd(t, mask, algo)
+        torch.cuda.synchronize()
+        check_grads(got, ref, dtype, f"128 mask {mask} {ALGO_NAMES[algo]}")
+
+
+@pytest.mark.parametrize("planes", [1, 257, 600])
+def test_bwd_128_planes_per_workgroup_counts(planes):
+    """More and fewer planes than compute units: each workgroup walks its share."""
+    print(f"[bwd] 128x128 planes={planes}", flush=True)
+    t = synth.random_general((1, planes, 128, 128), 4, device=DEV, seed=planes)
+    t = {k: v.to(torch.bfloat16) for k, v in t.items()}
+    got = run_bwd(t, 0xF, L.GSPN_ALGO_AUTO)
+    torch.cuda.synchronize()
+    idx = sorted({0, planes // 2, planes - 1})
+    for c in idx:
+        sub = {k: (v[:, :, :, c:c + 1] if k == "w" else v[:, c:c + 1]) for k, v in t.items()}
+        sel = [g[:, c:c + 1] if i != 1 else g[:, :, :, c:c + 1] for i, g in enumerate(got)]
+        check_grads(sel, oracle_bwd(sub, 0xF), torch.bfloat16, f"plane {c} of {planes}")
+    a = run_bwd(t, 0xF, L.GSPN_ALGO_AUTO)
+    torch.cuda.synchronize()
+    for u, v in zip(a, got):
+        assert torch.equal(u.view(torch.int16), v.view(torch.int16))
