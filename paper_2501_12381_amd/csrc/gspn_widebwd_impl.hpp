@@ -15,13 +15,13 @@
 //   P0  all waves: A = lam * x (a quarter of the rows each)
 //   F   wave d: forward recompute of h_d (weights streamed from HBM, lam * x
 //       from A), kept in registers
-//   Sh  B = sum_d h_d, the waves adding in direction order (one barrier each)
+//   Sh  B = sum_d h_d in a fixed order (four rounds, two waves each)
 //   P2  all waves: du = dy * B, A = u * dy
 //   A   wave d: adjoint g(line) = u*dy + transposed stencil of the next line's
 //       weights and g; dw_k = g * h(previous line)(p + k - 1).  The vertical
 //       waves store dw rows directly; the horizontal waves stage dw in LDS and
 //       write it out as row segments every SC columns
-//   Sg  B = sum_d g_d in direction order
+//   Sg  B = sum_d g_d in the same fixed order
 //   P4  all waves: dx = lam * B, dlam = x * B
 // Every sum has a fixed order, so results are reproducible run to run.
 //
@@ -46,7 +46,7 @@ struct WideBwdCfg {
   static constexpr int NP = 2;                     // positions per lane
   static constexpr int P = S + 1;                  // LDS row pitch (odd)
   static constexpr int ARR = S * P;                // floats per array
-  static constexpr int RV = 10;                    // vertical ring: rows in flight
+  static constexpr int RV = 14;                    // vertical ring: rows in flight
   static constexpr int VE = 16 / (int)sizeof(T);   // columns per 16-byte vector
   static constexpr int CG = 3;                     // horizontal ring: column groups of VE columns
   static constexpr int SC = 64 / (int)sizeof(T);   // horizontal dw staging: columns per flush (64 bytes)
@@ -361,109 +361,133 @@ __device__ __forceinline__ void wb_horizontal(const WideBwdParams& p, int64_t pl
 // The sum over directions into B, in direction order: round d adds wave d's
 // registers (stores when d is the first present direction).  Absent
 // directions keep the rounds' barriers in step.
-// Lines go in batches of 8 (reads, then writes) with scheduling barriers
-// between batches, so no more than a batch of reads is in flight in registers
-// beside the 256 of state.
-template <bool HZ>
-__device__ __forceinline__ void wb_sum_round(float* __restrict__ B, const float (&hreg)[128][2], int lane,
-                                             bool first) {
-  constexpr int P = 129, BT = 8;
-  static_for<0, 128 / BT>([&](auto bc) __attribute__((always_inline)) {
-    constexpr int l0 = decltype(bc)::value * BT;
-    float t[BT][2];
-    if (!first) {
+// The sums over directions go into B (zeroed first) in four rounds with a
+// barrier after each; in a round two waves of one kind add disjoint halves of
+// their lines (rows for the vertical waves, columns for the horizontal ones):
+//   round 0: T2B rows [0, 64), B2T rows [64, 128); round 1: the other halves;
+//   round 2: L2R columns [0, 64), R2L columns [64, 128); round 3: the others.
+// So every element receives its terms in a fixed order.  Lines go in batches
+// of BT, the reads of the next batch issued before the writes of the current.
+template <bool HZ, int L0>
+__device__ __forceinline__ void wb_sum_half(float* __restrict__ B, const float (&hreg)[128][2], int lane) {
+  constexpr int P = 129, BT = 16, NB = 64 / BT;
+  auto off = [&](int line) { return HZ ? (2 * lane) * P + line : line * P + 2 * lane; };
+  constexpr int O1 = HZ ? P : 1;
+  float t[2][BT][2];
+  static_for<0, BT>([&](auto jc) __attribute__((always_inline)) {
+    constexpr int line = L0 + decltype(jc)::value;
+    t[0][line - L0][0] = B[off(line)];
+    t[0][line - L0][1] = B[off(line) + O1];
+  });
+  static_for<0, NB>([&](auto bc) __attribute__((always_inline)) {
+    constexpr int b = decltype(bc)::value, cur = b & 1;
+    if constexpr (b + 1 < NB) {
       static_for<0, BT>([&](auto jc) __attribute__((always_inline)) {
-        constexpr int line = l0 + decltype(jc)::value;
-        const int o0 = HZ ? (2 * lane) * P + line : line * P + 2 * lane;
-        t[line - l0][0] = B[o0];
-        t[line - l0][1] = B[o0 + (HZ ? P : 1)];
+        constexpr int j = decltype(jc)::value, line = L0 + (b + 1) * BT + j;
+        t[cur ^ 1][j][0] = B[off(line)];
+        t[cur ^ 1][j][1] = B[off(line) + O1];
       });
     }
     static_for<0, BT>([&](auto jc) __attribute__((always_inline)) {
-      constexpr int line = l0 + decltype(jc)::value;
-      const int o0 = HZ ? (2 * lane) * P + line : line * P + 2 * lane;
-      B[o0] = first ? hreg[line][0] : t[line - l0][0] + hreg[line][0];
-      B[o0 + (HZ ? P : 1)] = first ? hreg[line][1] : t[line - l0][1] + hreg[line][1];
+      constexpr int j = decltype(jc)::value, line = L0 + b * BT + j;
+      B[off(line)] = t[cur][j][0] + hreg[line][0];
+      B[off(line) + O1] = t[cur][j][1] + hreg[line][1];
     });
     __builtin_amdgcn_sched_barrier(0);
   });
 }
 
-// Elementwise passes over the rows [32 wave, 32 wave + 32), in batches of 8
-// rows whose loads are issued before their use.
+// B = sum over the present directions of the waves' registers (B zeroed before).
+template <int D>
+__device__ __forceinline__ void wb_sum_rounds(float* __restrict__ B, const float (&hreg)[128][2], int lane,
+                                              bool present) {
+  constexpr bool HZ = D >= 2;
+  constexpr int first_half = (D & 1) ? 64 : 0;  // round 2k: the lower-numbered wave takes lines [0, 64)
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    if (present && (r >> 1) == (HZ ? 1 : 0)) {
+      if ((r & 1) == 0) wb_sum_half<HZ, first_half>(B, hreg, lane);
+      else wb_sum_half<HZ, 64 - first_half>(B, hreg, lane);
+    }
+    lds_barrier();
+  }
+}
+
+// Zero this wave's quarter of an LDS array.
+__device__ __forceinline__ void wb_zero_quarter(float* __restrict__ B, int wave, int lane) {
+  constexpr int N = 128 * 129, Q = (N + 3) / 4;
+  const int lo = wave * Q, hi = lo + Q < N ? lo + Q : N;
+  for (int i = lo + lane; i < hi; i += 64) B[i] = 0.f;
+}
+
+// Elementwise passes over the rows [32 wave, 32 wave + 32).  lam * x loads
+// and uses its rows in batches; the du and dx passes take their 32 rows of
+// operands loaded earlier (issued before the sum rounds, which need no memory,
+// so their latency passes under the rounds).
 template <typename T>
 struct WbRows {
-  static constexpr int S = 128, P = 129, RB = S * (int)sizeof(T), PB = S * RB, BT = 8;
+  static constexpr int S = 128, P = 129, RB = S * (int)sizeof(T), PB = S * RB, BT = 8, NR = 32;
+  typedef Pack<T, 2> PK;
   // A = lam * x
   __device__ __forceinline__ static void lamx(const WideBwdParams& p, int64_t pof, float* __restrict__ A, int wave,
                                               int lane) {
     const wide_rsrc_t rx = wide_rsrc((const T*)p.x + pof, PB), rl = wide_rsrc((const T*)p.lam + pof, PB);
     const int vo = 2 * lane * (int)sizeof(T);
 #pragma unroll
-    for (int b0 = 0; b0 < 32; b0 += BT) {
-      Pack<T, 2> vx[BT], vl[BT];
+    for (int b0 = 0; b0 < NR; b0 += BT) {
+      PK vx[BT], vl[BT];
 #pragma unroll
       for (int j = 0; j < BT; ++j) {
-        wide_load(vx[j], rx, vo, (32 * wave + b0 + j) * RB);
-        wide_load(vl[j], rl, vo, (32 * wave + b0 + j) * RB);
+        wide_load(vx[j], rx, vo, (NR * wave + b0 + j) * RB);
+        wide_load(vl[j], rl, vo, (NR * wave + b0 + j) * RB);
       }
 #pragma unroll
       for (int j = 0; j < BT; ++j) {
-        const int o = (32 * wave + b0 + j) * P + 2 * lane;
+        const int o = (NR * wave + b0 + j) * P + 2 * lane;
         A[o] = vl[j].get(0) * vx[j].get(0);
         A[o + 1] = vl[j].get(1) * vx[j].get(1);
       }
       __builtin_amdgcn_sched_barrier(0);
     }
   }
-  // du = dy * B, A = u * dy
+  // the wave's rows of two maps
+  __device__ __forceinline__ static void fetch(const void* ma, const void* mb, int64_t pof, PK (&va)[NR],
+                                               PK (&vb)[NR], int wave, int lane) {
+    const wide_rsrc_t ra = wide_rsrc((const T*)ma + pof, PB), rb = wide_rsrc((const T*)mb + pof, PB);
+    const int vo = 2 * lane * (int)sizeof(T);
+#pragma unroll
+    for (int j = 0; j < NR; ++j) {
+      wide_load(va[j], ra, vo, (NR * wave + j) * RB);
+      wide_load(vb[j], rb, vo, (NR * wave + j) * RB);
+    }
+  }
+  // du = dy * B, A = u * dy   (vd = dy, vu = u)
   __device__ __forceinline__ static void dudy(const WideBwdParams& p, int64_t pof, float* __restrict__ A,
-                                              const float* __restrict__ B, int wave, int lane) {
-    const wide_rsrc_t rdy = wide_rsrc((const T*)p.dy + pof, PB), ru = wide_rsrc((const T*)p.u + pof, PB);
+                                              const float* __restrict__ B, const PK (&vd)[NR], const PK (&vu)[NR],
+                                              int wave, int lane) {
     const wide_rsrc_t rdu = wide_rsrc((T*)p.du + pof, PB);
     const int vo = 2 * lane * (int)sizeof(T);
 #pragma unroll
-    for (int b0 = 0; b0 < 32; b0 += BT) {
-      Pack<T, 2> vd[BT], vu[BT];
-#pragma unroll
-      for (int j = 0; j < BT; ++j) {
-        wide_load(vd[j], rdy, vo, (32 * wave + b0 + j) * RB);
-        wide_load(vu[j], ru, vo, (32 * wave + b0 + j) * RB);
-      }
-#pragma unroll
-      for (int j = 0; j < BT; ++j) {
-        const int r = 32 * wave + b0 + j, o = r * P + 2 * lane;
-        const float du[2] = {vd[j].get(0) * B[o], vd[j].get(1) * B[o + 1]};
-        wide_store<T, 2>(du, rdu, vo, r * RB);
-        A[o] = vu[j].get(0) * vd[j].get(0);
-        A[o + 1] = vu[j].get(1) * vd[j].get(1);
-      }
-      __builtin_amdgcn_sched_barrier(0);
+    for (int j = 0; j < NR; ++j) {
+      const int r = NR * wave + j, o = r * P + 2 * lane;
+      const float du[2] = {vd[j].get(0) * B[o], vd[j].get(1) * B[o + 1]};
+      wide_store<T, 2>(du, rdu, vo, r * RB);
+      A[o] = vu[j].get(0) * vd[j].get(0);
+      A[o + 1] = vu[j].get(1) * vd[j].get(1);
     }
   }
-  // dx = lam * B, dlam = x * B
+  // dx = lam * B, dlam = x * B   (vl = lam, vx = x)
   __device__ __forceinline__ static void dxdl(const WideBwdParams& p, int64_t pof, const float* __restrict__ B,
-                                              int wave, int lane) {
-    const wide_rsrc_t rl = wide_rsrc((const T*)p.lam + pof, PB), rx = wide_rsrc((const T*)p.x + pof, PB);
+                                              const PK (&vl)[NR], const PK (&vx)[NR], int wave, int lane) {
     const wide_rsrc_t rdx = wide_rsrc((T*)p.dx + pof, PB), rdl = wide_rsrc((T*)p.dlam + pof, PB);
     const int vo = 2 * lane * (int)sizeof(T);
 #pragma unroll
-    for (int b0 = 0; b0 < 32; b0 += BT) {
-      Pack<T, 2> vl[BT], vx[BT];
-#pragma unroll
-      for (int j = 0; j < BT; ++j) {
-        wide_load(vl[j], rl, vo, (32 * wave + b0 + j) * RB);
-        wide_load(vx[j], rx, vo, (32 * wave + b0 + j) * RB);
-      }
-#pragma unroll
-      for (int j = 0; j < BT; ++j) {
-        const int r = 32 * wave + b0 + j, o = r * P + 2 * lane;
-        const float dx[2] = {vl[j].get(0) * B[o], vl[j].get(1) * B[o + 1]};
-        const float dl[2] = {vx[j].get(0) * B[o], vx[j].get(1) * B[o + 1]};
-        wide_store<T, 2>(dx, rdx, vo, r * RB);
-        wide_store<T, 2>(dl, rdl, vo, r * RB);
-      }
-      __builtin_amdgcn_sched_barrier(0);
+    for (int j = 0; j < NR; ++j) {
+      const int r = NR * wave + j, o = r * P + 2 * lane;
+      const float dx[2] = {vl[j].get(0) * B[o], vl[j].get(1) * B[o + 1]};
+      const float dl[2] = {vx[j].get(0) * B[o], vx[j].get(1) * B[o + 1]};
+      wide_store<T, 2>(dx, rdx, vo, r * RB);
+      wide_store<T, 2>(dl, rdl, vo, r * RB);
     }
   }
 };
@@ -475,44 +499,58 @@ template <typename T, int D>
 __device__ __forceinline__ void wide_bwd_wave(const WideBwdParams& p, float* __restrict__ A, float* __restrict__ B,
                                               int lane0) {
   using C = WideBwdCfg<T>;
+  using RW = WbRows<T>;
   constexpr int S = C::S;
   constexpr bool HZ = D >= 2, REV = D & 1;
   const int slot = p.slot[D];
-  int first_dir = 0;
-  while (first_dir < 4 && p.slot[first_dir] < 0) ++first_dir;
+  const bool present = slot >= 0;
   uint32_t* stg = reinterpret_cast<uint32_t*>(B) + (HZ ? (D - 2) * C::SREG : 0);
   float hreg[128][2];
+  typename RW::PK va[RW::NR], vb[RW::NR];
   for (int64_t plane = blockIdx.x; plane < p.planes; plane += gridDim.x) {
     // the lane index is made opaque per plane, so the compiler cannot hoist
     // the (many) per-line addresses out of the plane loop and keep them live
     int lane = lane0;
     asm volatile("" : "+v"(lane));
     const int64_t pof = plane * (S * S);
-    WbRows<T>::lamx(p, pof, A, D, lane);
+    // STAMP(0)
+    RW::lamx(p, pof, A, D, lane);
+    // STAMP(1)
     lds_barrier();
-    if (slot >= 0) {
+    // STAMP(2)
+    wb_zero_quarter(B, D, lane);  // the sums' array (free until the sum rounds)
+    if (present) {
       if constexpr (HZ) wb_horizontal<T, REV>(p, plane, slot, hreg, A, stg, p.gstart[D], lane, true);
       else wb_vertical<T, REV>(p, plane, slot, hreg, A, p.gstart[D], lane, true);
     }
+    int lf = lane;
+    asm volatile("" : "+v"(lf));  // keeps the loads below after the scan
+    RW::fetch(p.dy, p.u, pof, va, vb, D, lf);  // operands of the du pass
+    // STAMP(3)
     lds_barrier();
-#pragma unroll
-    for (int d = 0; d < 4; ++d) {
-      if (d == D && slot >= 0) wb_sum_round<HZ>(B, hreg, lane, D == first_dir);
-      lds_barrier();
-    }
-    WbRows<T>::dudy(p, pof, A, B, D, lane);
+    // STAMP(4)
+    wb_sum_rounds<D>(B, hreg, lane, present);  // B = sum_d h_d
+    // STAMP(5)
+    RW::dudy(p, pof, A, B, va, vb, D, lane);
+    // STAMP(6)
     lds_barrier();
-    if (slot >= 0) {
+    // STAMP(7)
+    if (present) {
       if constexpr (HZ) wb_horizontal<T, REV>(p, plane, slot, hreg, A, stg, p.gstart[D], lane, false);
       else wb_vertical<T, REV>(p, plane, slot, hreg, A, p.gstart[D], lane, false);
     }
+    lf = lane;
+    asm volatile("" : "+v"(lf));
+    RW::fetch(p.lam, p.x, pof, va, vb, D, lf);  // operands of the dx pass
+    // STAMP(8)
+    lds_barrier();  // the horizontal waves' staging in B is written out
+    wb_zero_quarter(B, D, lane);
     lds_barrier();
-#pragma unroll
-    for (int d = 0; d < 4; ++d) {
-      if (d == D && slot >= 0) wb_sum_round<HZ>(B, hreg, lane, D == first_dir);
-      lds_barrier();
-    }
-    WbRows<T>::dxdl(p, pof, B, D, lane);
+    // STAMP(9)
+    wb_sum_rounds<D>(B, hreg, lane, present);  // B = sum_d g_d
+    // STAMP(10)
+    RW::dxdl(p, pof, B, va, vb, D, lane);
+    // STAMP(11)
     // the next plane's first pass writes only A (last read before the adjoint's
     // barrier); B is written again only after its forward barrier
   }
