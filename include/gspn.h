@@ -121,14 +121,19 @@ enum {
   GSPN_ALGO_RESIDENT = 1, /* whole plane kept on chip, all directions in one kernel */
   GSPN_ALGO_STREAM = 2,   /* one pass per direction through an fp32 workspace */
   GSPN_ALGO_RESIDENT_GENERIC = 3, /* resident family without size-specialised kernels */
-  GSPN_ALGO_TWO_PASS = 4 /* forward only, for planes too large to keep on chip: the
+  GSPN_ALGO_TWO_PASS = 4 /* for planes too large to keep on chip.  Forward: the
                             vertical directions in one pass, the horizontal pair in
                             blocks of 128-byte columns, partial sums in an fp32
                             workspace (two B*C*H*W arrays when both vertical
                             directions and a horizontal one are in the mask, one
-                            otherwise).  Needs W * element size a multiple of
-                            16 bytes and at least 128 bytes, W <= 4096 (bf16) or
-                            2048 (f32), and 16-byte aligned x, w, lam, u, y. */
+                            otherwise).  Backward (a horizontal direction in the
+                            mask): each horizontal direction recomputes its h into
+                            the workspace block by block, then runs the adjoint over
+                            the blocks in reverse order; vertical directions stream.
+                            Workspace: three fp32 B*C*H*W arrays and 6*B*C*H floats.
+                            Needs W * element size a multiple of 16 bytes and at
+                            least 128 bytes, W <= 4096 (bf16) or 2048 (f32), and
+                            16-byte aligned tensors (AUTO falls back to streaming). */
 };
 
 /* Bytes of workspace gspn_scan_fwd needs for this problem (0 if none). */
@@ -171,8 +176,9 @@ int gspn_scan_fwd_noalloc(const void* x, const void* w, const void* lam, const v
 
 /* Bytes of workspace gspn_scan_bwd needs for this problem (0 if none).  With
  * GSPN_ALGO_AUTO the size covers every pointer alignment: AUTO runs the
- * streaming family, which needs a workspace, when a tensor the resident
- * kernels would read or write as 16-byte vectors is only element-aligned. */
+ * streaming family, which needs a workspace (never more than the two-pass
+ * one), when a tensor the resident or two-pass kernels would read or write as
+ * 16-byte vectors is only element-aligned. */
 size_t gspn_scan_bwd_workspace_bytes(int64_t B, int64_t C, int64_t H, int64_t W, uint32_t mask,
                                      gspn_dtype dtype, int64_t group_h, int64_t group_w,
                                      uint32_t flags, int algo);

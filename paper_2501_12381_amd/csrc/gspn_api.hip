@@ -75,6 +75,7 @@ struct Problem {
   bool empty;
   int gh, gw;                       // group lengths, 0 when the scan is global on that axis
   uint32_t flags;
+  uint32_t mask;
   bool grouped() const { return gh > 0 || gw > 0; }
   bool lam_pd() const { return flags & GSPN_FLAG_LAM_PER_DIR; }
   bool u_pd() const { return flags & GSPN_FLAG_U_PER_DIR; }
@@ -91,6 +92,7 @@ int check_shape(int64_t B, int64_t C, int64_t H, int64_t W, uint32_t mask, int d
   if ((flags & GSPN_FLAG_EDGE_RENORM) && !(flags & GSPN_FLAG_W_LOGITS)) return GSPN_ERR_UNSUPPORTED;
   if (group_h < 0 || group_w < 0) return GSPN_ERR_UNSUPPORTED;
   p->flags = flags;
+  p->mask = mask;
   // a group at least as long as the axis is the global scan
   p->gh = (group_h == 0 || group_h >= H) ? 0 : (int)group_h;
   p->gw = (group_w == 0 || group_w >= W) ? 0 : (int)group_w;
@@ -157,7 +159,10 @@ bool resident_fits(const Problem& p, int dtype, bool backward) {
 
 bool two_pass_fits(const Problem& p, int dtype, bool backward) {
   if (p.flags || (p.grouped() && !kTwoPassGroups)) return false;
-  return !backward && gspn::large_fwd_fits((int)p.H, (int)p.W, dtype);
+  // the backward runs its horizontal directions on the two-pass kernels
+  // (their vertical ones on the streaming kernels)
+  if (backward && !(p.mask & (DIR_L2R | DIR_R2L))) return false;
+  return gspn::large_fwd_fits((int)p.H, (int)p.W, dtype);
 }
 
 int choose_algo(const Problem& p, int dtype, int algo, bool backward) {
@@ -190,8 +195,14 @@ size_t fwd_ws_bytes(const Problem& p, int algo, uint32_t mask) {
   return 0;
 }
 
+// streaming and two-pass backward: h of one direction (the previous line's
+// for the streaming kernels), the running sums of h and g (fp32); the
+// two-pass kernels add the column state of their horizontal launches
 size_t bwd_ws_bytes(const Problem& p, int algo) {
   if (algo == GSPN_ALGO_STREAM) return 3 * round_up((size_t)p.npc * 4, kWsAlign);
+  if (algo == GSPN_ALGO_TWO_PASS)
+    return 3 * round_up((size_t)p.npc * 4, kWsAlign) +
+           round_up((size_t)gspn::large_bwd_state_floats(p.planes, (int)p.H) * 4, kWsAlign);
   return 0;
 }
 
@@ -334,8 +345,8 @@ int gspn_scan_bwd(const void* dy, const void* x, const void* w, const void* lam,
   if (st != GSPN_OK) return st;
   int a = choose_algo(p, dtype, algo, true);
   if (a < 0) return GSPN_ERR_UNSUPPORTED;
-  if (a == GSPN_ALGO_RESIDENT || a == GSPN_ALGO_RESIDENT_GENERIC) {
-    // the resident backward reads and writes 16-byte vectors
+  if (a == GSPN_ALGO_RESIDENT || a == GSPN_ALGO_RESIDENT_GENERIC || a == GSPN_ALGO_TWO_PASS) {
+    // the resident and two-pass backward kernels read and write 16-byte vectors
     for (const void* q : {dy, x, w, lam, u, (const void*)dx, (const void*)dw, (const void*)dlam, (const void*)du})
       if ((uintptr_t)q % 16) {
         if (algo != GSPN_ALGO_AUTO) return GSPN_ERR_ALIGN;
@@ -369,6 +380,22 @@ int gspn_scan_bwd(const void* dy, const void* x, const void* w, const void* lam,
     const void* lam_i = (const char*)lam + (p.lam_pd() ? i * tb : 0);
     const void* u_i = (const char*)u + (p.u_pd() ? i * tb : 0);
     const int group = (ds[i] == DIR_T2B || ds[i] == DIR_B2T) ? p.gh : p.gw;
+    if (a == GSPN_ALGO_TWO_PASS && (ds[i] == DIR_L2R || ds[i] == DIR_R2L)) {
+      LargeBwdHArgs l{};
+      l.x = x; l.lam = lam; l.dy = dy; l.u = u;
+      l.w = (const char*)w + (size_t)i * 3 * tb;
+      l.dw = (char*)dw + (size_t)i * 3 * tb;
+      l.hbuf = hprev; l.hsum = hsum; l.gsum = gsum;
+      l.state = (float*)((char*)workspace + 3 * fb);
+      l.first = i == 0;
+      l.dir = ds[i] == DIR_R2L ? 1 : 0;
+      l.planes = p.planes; l.H = (int)H; l.W = (int)W;
+      l.group = group;
+      l.stream = stream;
+      st = hip_status(large_bwd_h(l, dtype));
+      if (st != GSPN_OK) return st;
+      continue;
+    }
     StreamFwdArgs f{};
     f.x = x; f.lam = lam_i; f.u = nullptr; f.y = nullptr;
     f.w = (const char*)w + (size_t)i * 3 * tb;

@@ -1,0 +1,357 @@
+// Backward of the horizontal directions for planes too large to keep on chip
+// (e.g. 2048 x 2048): the exact adjoint of Eq. 1 along columns, one direction
+// at a time, in two launch sequences over blocks of K columns (K = 128 bytes
+// of a row, the block of the forward's pass H):
+//
+//   recompute  large_h_kernel in its `rec` mode, blocks in scan order: h of
+//              the direction into an fp32 plane `hbuf`, and hsum (+)= h.
+//   adjoint    large_hadj_kernel below, blocks in reverse scan order.  A
+//              workgroup owns a band of rows plus a halo of K rows on each
+//              side (one row per lane), as in the forward: starting from the
+//              exact products of the column after the block (carried between
+//              launches in a small workspace), the transposed stencil
+//                g[l][p] = u dy[l][p] + w0[n][p+1] g[n][p+1] + w1[n][p] g[n][p]
+//                          + w2[n][p-1] g[n][p-1]          (n: the next line)
+//              leaves the band exact after K columns.  The band's rows of the
+//              block's h (and one row above and below) sit in LDS;
+//                dw_k[l][p] = g[l][p] h[prev][p+k-1]
+//              is formed per step in registers and stored as 128-byte row
+//              segments; g replaces the h column that no later step reads and
+//              is added to gsum with coalesced accesses at the end.
+//
+// The row segments of dy, u and the three weight maps come in as one register
+// tile per launch, like the forward's; the dw words are produced as the tile
+// words die, so the two share the register budget.
+#pragma once
+
+#include "gspn_large_impl.hpp"
+
+namespace gspn {
+
+struct LargeHAdjParams {
+  const void* dy;
+  const void* u;
+  const void* w;       // this direction's w0 (w1, w2 at +npc, +2 npc)
+  void* dw;            // this direction's dw0 (dw1, dw2 at +npc, +2 npc)
+  const float* hbuf;   // h of this direction (fp32)
+  float* gsum;         // fp32 running sum of g over the directions
+  float* state;        // [2 parities][3][planes * H]: w_k * g of the last column done
+  int64_t planes, npc;
+  int H, W;
+  int first;           // store gsum instead of adding
+  int step, nblk;
+  int band_rows, nbands, halo;
+  // bit i: window column i takes nothing from the next line (that line starts
+  // a group); bit i of gmask: window column i starts a group (zero previous state)
+  uint64_t zmask, gmask;
+};
+
+// DIR 0: left-to-right (its adjoint walks the blocks and columns right to left);
+// DIR 1: right-to-left (adjoint left to right).
+template <typename T, int NW, int DIR>
+__global__ void __launch_bounds__(64 * NW) large_hadj_kernel(LargeHAdjParams p) {
+  using C = LargeCfg<T>;
+  constexpr int K = C::KH, HV = C::HV, VE = C::VE;
+  constexpr int HC = K + 4;           // h columns in LDS: the window and 4 on its scan-previous side
+  constexpr int HP = HC + 1;          // LDS pitch (odd: column accesses hit distinct banks)
+  constexpr int HOFF = DIR ? 0 : 4;   // LDS column of window column 0
+  constexpr int PREV = DIR ? 1 : -1;  // window offset of the scan-previous column
+  typedef Pack<T, VE> PK;
+  extern __shared__ float lds[];      // [band_rows + 2][HP]; edges [2][NW][2]; 64 dummy slots
+  float* edge = lds + (p.band_rows + 2) * HP;
+
+  // workgroup -> (plane, band); the bands of a plane share an XCD
+  const int64_t G = gridDim.x, b = blockIdx.x;
+  const int64_t G8 = G / 8 * 8;
+  const int64_t id = b < G8 ? (b % 8) * (G8 / 8) + b / 8 : b;
+  const int band = (int)(id % p.nbands);
+  const int64_t plane = id / p.nbands;
+  const int blk = DIR ? p.step : p.nblk - 1 - p.step;
+  const int H = p.H, W = p.W;
+  const int c0 = blk * K;
+  const int ws = c0 + K <= W ? c0 : W - K;
+  const int lo = c0 - ws;  // first window column of this block
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int used = p.band_rows + 2 * p.halo;
+  const int r = band * p.band_rows - p.halo + (tid < used ? tid : used - 1);
+  const bool row_ok = tid < used && r >= 0 && r < H;
+  const int rc = r < 0 ? 0 : (r >= H ? H - 1 : r);
+  const int br = tid - p.halo;
+  const bool in_band = br >= 0 && br < p.band_rows && row_ok;
+  const int rows = min(p.band_rows, H - band * p.band_rows);  // band rows inside the plane
+
+  const int64_t HW = (int64_t)H * W;
+  const int64_t rb = plane * HW + (int64_t)rc * W + ws;
+  const T* wb = (const T*)p.w;
+  const T* base[5] = {(const T*)p.dy + rb, (const T*)p.u + rb, wb + rb, wb + p.npc + rb, wb + 2 * p.npc + rb};
+
+  // the register tile: dy, u, w0, w1, w2 of the lane's row over the window,
+  // map by map, each row segment's vectors back to back
+  PK tile[5][HV];
+#pragma unroll
+  for (int m = 0; m < 5; ++m) {
+#pragma unroll
+    for (int i = 0; i < HV; ++i) tile[m][i].load(base[m] + i * VE);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  // h of the band rows and one row on each side, window columns shifted by
+  // HOFF, into LDS (zero outside the plane)
+  {
+    constexpr int NV = HC / 4;  // float4 vectors per LDS row
+    const int nrow = p.band_rows + 2;
+    const int nvec = nrow * NV;
+    const int r0 = band * p.band_rows - 1;
+    const int cb = ws - HOFF;
+    const float* hp0 = p.hbuf + plane * HW;
+    constexpr int TT = 64 * NW, UB = 4;
+    for (int e0 = tid; e0 < nvec; e0 += TT * UB) {
+      float4 v[UB];
+#pragma unroll
+      for (int k = 0; k < UB; ++k) {
+        const int e = e0 + k * TT;
+        const int rr = e / NV, cv = e - rr * NV;
+        const int gr = r0 + rr, gc = cb + cv * 4;
+        const bool ok = e < nvec && gr >= 0 && gr < H && gc >= 0 && gc < W;
+        v[k] = ok ? *reinterpret_cast<const float4*>(hp0 + (int64_t)gr * W + gc) : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+#pragma unroll
+      for (int k = 0; k < UB; ++k) {
+        const int e = e0 + k * TT;
+        if (e < nvec) {
+          const int rr = e / NV, cv = e - rr * NV;
+          float* d = lds + rr * HP + cv * 4;
+          d[0] = v[k].x; d[1] = v[k].y; d[2] = v[k].z; d[3] = v[k].w;
+        }
+      }
+    }
+  }
+
+  // products of the column after the block (scan order), from the previous launch
+  float a0 = 0.f, a1 = 0.f, a2 = 0.f;
+  const int64_t sp = plane * H;
+  const int64_t sst = p.planes * H;
+  if (p.step > 0) {
+    const float* sin = p.state + (int64_t)((p.step - 1) & 1) * 3 * sst + sp + rc;
+    a0 = sin[0];
+    a1 = sin[sst];
+    a2 = sin[2 * sst];
+  }
+  if (!row_ok) a0 = a1 = a2 = 0.f;
+  // wave edges: lane 0 publishes its a0 (row above it reads it), lane 63 its a2
+  if (lane == 0) edge[(1 * NW + wave) * 2 + 0] = a0;
+  if (lane == 63) edge[(1 * NW + wave) * 2 + 1] = a2;
+  auto eslot = [&](int par) {
+    return lane == 0 ? (par * NW + wave) * 2 : (lane == 63 ? (par * NW + wave) * 2 + 1 : 4 * NW + lane);
+  };
+  const int eo0 = eslot(0), eo1 = eslot(1);
+  float* hrow = lds + (in_band ? br + 1 : 1) * HP;  // this row's h (then g) in LDS
+
+  // dw words: bf16 pairs (or fp32) per map and column, filled as the steps go
+  constexpr int DWW = PK::kWords * HV;
+  uint32_t dwv[3][DWW];
+  float pend[3] = {0.f, 0.f, 0.f};
+  const uint64_t zm = p.zmask, gm = p.gmask;
+  lds_barrier();  // h and the initial edges are in LDS
+
+  auto step = [&](auto ic) __attribute__((always_inline)) {
+    constexpr int i = decltype(ic)::value;
+    constexpr int ti = DIR ? i : K - 1 - i;  // window column of this step
+    if (ti < lo) return;                     // columns of the next block (uniform)
+    const int par = i & 1;
+    const bool zr = (zm >> ti) & 1;
+    float an = from_next_lane(a0), ap = from_prev_lane(a2);
+    if constexpr (NW > 1) {
+      const float nd = edge[((par ^ 1) * NW + (wave < NW - 1 ? wave + 1 : wave)) * 2 + 0];
+      const float nu = edge[((par ^ 1) * NW + (wave > 0 ? wave - 1 : wave)) * 2 + 1];
+      if (lane == 63) an = wave < NW - 1 ? nd : 0.f;
+      if (lane == 0) ap = wave > 0 ? nu : 0.f;
+    }
+    float gin = a1 + an + ap;
+    gin = zr ? 0.f : gin;
+    const float dyv = tile[0][ti / VE].get(ti % VE), uv = tile[1][ti / VE].get(ti % VE);
+    float g = fmaf(uv, dyv, gin);
+    g = row_ok ? g : 0.f;
+    a0 = tile[2][ti / VE].get(ti % VE) * g;
+    a1 = tile[3][ti / VE].get(ti % VE) * g;
+    a2 = tile[4][ti / VE].get(ti % VE) * g;
+    edge[par ? eo1 : eo0] = lane == 0 ? a0 : a2;
+    // dw from the previous column's h on rows p-1, p, p+1 (zero at a group start)
+    const bool gr = (gm >> ti) & 1;
+    const int hc = ti + HOFF + PREV;
+    const float hl = gr ? 0.f : hrow[hc - HP], hm = gr ? 0.f : hrow[hc], hr = gr ? 0.f : hrow[hc + HP];
+    const float d0 = g * hl, d1 = g * hm, d2 = g * hr;
+    if constexpr (sizeof(T) == 2) {
+      // a word holds columns 2j (low half) and 2j + 1; the second one done completes it
+      constexpr bool second = DIR ? (ti & 1) : !(ti & 1);
+      if constexpr (!second) {
+        pend[0] = d0; pend[1] = d1; pend[2] = d2;
+      } else {
+        constexpr int wi = ti / 2;
+        if constexpr (DIR) {
+          dwv[0][wi] = pack_bf2(pend[0], d0); dwv[1][wi] = pack_bf2(pend[1], d1); dwv[2][wi] = pack_bf2(pend[2], d2);
+        } else {
+          dwv[0][wi] = pack_bf2(d0, pend[0]); dwv[1][wi] = pack_bf2(d1, pend[1]); dwv[2][wi] = pack_bf2(d2, pend[2]);
+        }
+      }
+    } else {
+      dwv[0][ti] = __float_as_uint(d0); dwv[1][ti] = __float_as_uint(d1); dwv[2][ti] = __float_as_uint(d2);
+    }
+    if (in_band) hrow[ti + HOFF] = g;  // h of this column is read by no later step
+    lds_barrier();
+  };
+  static_for<0, K>([&](auto ic) __attribute__((always_inline)) { step(ic); });
+
+  // products of the last column for the next launch (band rows cover the plane)
+  if (in_band) {
+    float* so = p.state + (int64_t)(p.step & 1) * 3 * sst + sp + r;
+    so[0] = a0;
+    so[sst] = a1;
+    so[2 * sst] = a2;
+  }
+  // dw: the lane's row segments of the block's columns, 16 bytes at a time
+  if (in_band) {
+    T* d0p = (T*)p.dw + rb;
+#pragma unroll
+    for (int k = 0; k < 3; ++k)
+#pragma unroll
+      for (int v = 0; v < HV; ++v) {
+        if (v * VE < lo) continue;
+        uint4 q;
+        q.x = dwv[k][v * 4 + 0]; q.y = dwv[k][v * 4 + 1]; q.z = dwv[k][v * 4 + 2]; q.w = dwv[k][v * 4 + 3];
+        *reinterpret_cast<uint4*>(d0p + (int64_t)k * p.npc + v * VE) = q;
+      }
+  }
+  __syncthreads();
+
+  // gsum (+)= g over the band rows and the block's columns, 4 floats a thread
+  const int nvr = (K - lo) / 4;
+  const int n = rows * nvr;
+  const int64_t ob = plane * HW + (int64_t)band * p.band_rows * W + ws;
+  constexpr int TT = 64 * NW, U = 8;
+  for (int e0 = tid; e0 < n; e0 += TT * U) {
+    float av[U][4];
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      const int e = e0 + k * TT < n ? e0 + k * TT : e0;
+      const int rr = e / nvr, cc = lo + (e - rr * nvr) * 4;
+      if (!p.first) ldv<4>(p.gsum + ob + (int64_t)rr * W + cc, av[k]);
+    }
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      const int e = e0 + k * TT;
+      if (e < n) {
+        const int rr = e / nvr, cc = lo + (e - rr * nvr) * 4;
+        const float* gl = lds + (rr + 1) * HP + cc + HOFF;
+        float s[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) s[q] = (p.first ? 0.f : av[k][q]) + gl[q];
+        stv<4>(p.gsum + ob + (int64_t)rr * W + cc, s);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// host side
+// ---------------------------------------------------------------------------
+
+template <typename T, int NW>
+hipError_t launch_large_hadj_nw(const LargeHAdjParams& p, int dir, int64_t grid, size_t lds, hipStream_t st) {
+  auto kern = dir ? large_hadj_kernel<T, NW, 1> : large_hadj_kernel<T, NW, 0>;
+  if (lds > 64 * 1024) {
+    hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(64 * NW), lds, st, p);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_large_hadj(const LargeHAdjParams& p, int dir, int nw, int64_t grid, size_t lds, hipStream_t st) {
+  switch (nw) {
+    case 1: return launch_large_hadj_nw<T, 1>(p, dir, grid, lds, st);
+    case 2: return launch_large_hadj_nw<T, 2>(p, dir, grid, lds, st);
+    case 3: return launch_large_hadj_nw<T, 3>(p, dir, grid, lds, st);
+    case 4: return launch_large_hadj_nw<T, 4>(p, dir, grid, lds, st);
+    case 5: return launch_large_hadj_nw<T, 5>(p, dir, grid, lds, st);
+    case 6: return launch_large_hadj_nw<T, 6>(p, dir, grid, lds, st);
+    case 7: return launch_large_hadj_nw<T, 7>(p, dir, grid, lds, st);
+    case 8: return launch_large_hadj_nw<T, 8>(p, dir, grid, lds, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <typename T>
+hipError_t large_bwd_h_t(const LargeBwdHArgs& a) {
+  using C = LargeCfg<T>;
+  constexpr int K = C::KH;
+  if (!large_fwd_supported<T>(a.H, a.W)) return hipErrorInvalidValue;
+  const LargeGeom<T> g = large_geom<T>(a.H, a.W);
+  hipStream_t st = (hipStream_t)a.stream;
+  const int64_t npc = a.planes * (int64_t)a.H * a.W;
+  const int64_t grid = (int64_t)g.nbands * a.planes;
+  if (grid > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+  const int GW = (a.group > 0 && a.group < a.W) ? a.group : a.W;
+  // scan order: left-to-right visits column c after c - 1, right-to-left after c + 1
+  auto starts = [&](int c) { return a.dir ? ((c + 1) % GW == 0) : (c % GW == 0); };
+  auto window = [&](int blk) {
+    const int c0 = blk * K;
+    return c0 + K <= a.W ? c0 : a.W - K;
+  };
+
+  // recompute: h into hbuf, hsum (+)= h; blocks in scan order
+  LargeHParams h{};
+  h.x = a.x; h.lam = a.lam; h.w = a.w; h.u = nullptr; h.y = nullptr; h.acc = a.hsum; h.state = a.state;
+  h.planes = a.planes; h.npc = npc; h.H = a.H; h.W = a.W;
+  // the weight slot is 0: w points at this direction's three maps
+  h.slot0 = a.dir ? -1 : 0;
+  h.slot1 = a.dir ? 0 : -1;
+  h.nblk = g.nblk; h.delay = 0; h.half = 0;
+  h.band_rows = g.band_rows; h.nbands = g.nbands; h.halo = g.halo;
+  h.has_v = a.first ? 0 : 1;
+  h.acc_b = nullptr;
+  h.rec = 1;
+  h.hbuf = a.hbuf;
+  for (int j = 0; j < g.nblk; ++j) {
+    const int blk = a.dir ? g.nblk - 1 - j : j;
+    const int ws = window(blk);
+    uint64_t m = 0;
+    if (GW < a.W)
+      for (int i = 0; i < K; ++i)
+        if (starts(ws + i)) m |= 1ull << i;
+    h.step = j;
+    h.gmask[0] = a.dir ? 0 : m;
+    h.gmask[1] = a.dir ? m : 0;
+    hipError_t e = launch_large_h<T>(h, g.nw, grid, g.lds_h, st);
+    if (e != hipSuccess) return e;
+  }
+
+  // adjoint: blocks in reverse scan order
+  LargeHAdjParams p{};
+  p.dy = a.dy; p.u = a.u; p.w = a.w; p.dw = a.dw; p.hbuf = a.hbuf; p.gsum = a.gsum; p.state = a.state;
+  p.planes = a.planes; p.npc = npc; p.H = a.H; p.W = a.W;
+  p.first = a.first;
+  p.nblk = g.nblk;
+  p.band_rows = g.band_rows; p.nbands = g.nbands; p.halo = g.halo;
+  const size_t lds = ((size_t)(g.band_rows + 2) * (K + 5) + 4 * 8 + 64) * sizeof(float);
+  for (int j = 0; j < g.nblk; ++j) {
+    const int blk = a.dir ? j : g.nblk - 1 - j;
+    const int ws = window(blk);
+    uint64_t zm = 0, gm = 0;
+    if (GW < a.W)
+      for (int i = 0; i < K; ++i) {
+        const int c = ws + i, nxt = a.dir ? c - 1 : c + 1;
+        if (starts(c)) gm |= 1ull << i;
+        if (nxt >= 0 && nxt < a.W && starts(nxt)) zm |= 1ull << i;
+      }
+    p.step = j;
+    p.zmask = zm;
+    p.gmask = gm;
+    hipError_t e = launch_large_hadj<T>(p, a.dir, g.nw, grid, lds, st);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+}  // namespace gspn

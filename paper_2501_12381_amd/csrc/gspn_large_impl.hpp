@@ -328,6 +328,10 @@ struct LargeHParams {
   // local GSPN, per direction (left-to-right, right-to-left): bit i set when
   // window column i of this launch starts a group (the state restarts from zero)
   uint64_t gmask[2];
+  // recompute step of the backward (one direction): acc (+)= h, and h itself
+  // to hbuf; nothing is multiplied by u
+  int rec;
+  float* hbuf;
 };
 
 template <typename T, int NW>
@@ -395,7 +399,7 @@ __global__ void __launch_bounds__(64 * NW) large_h_kernel(LargeHParams p) {
   // during the last quarter of the scan (their tile registers are dead by
   // then), so the epilogue finds them in registers
   const bool second = both && p.step >= p.half;
-  const bool fin = !both || second;
+  const bool fin = !p.rec && (!both || second);
   const bool read_acc = second || p.has_v;
   const bool add_b = p.acc_b != nullptr && !second;  // the vertical sum still lives in two arrays
   const int rows = min(p.band_rows, H - band * p.band_rows);
@@ -481,6 +485,7 @@ __global__ void __launch_bounds__(64 * NW) large_h_kernel(LargeHParams p) {
     float s[VE];
 #pragma unroll
     for (int q = 0; q < VE; ++q) s[q] = (read_acc ? (add_b ? av[q] + bv[q] : av[q]) : 0.f) + lds[rr * KP + cc + q];
+    if (p.rec) stv<VE>(p.hbuf + o, lds + rr * KP + cc);
     if (fin) {
 #pragma unroll
       for (int q = 0; q < VE; ++q) s[q] *= uv.get(q);

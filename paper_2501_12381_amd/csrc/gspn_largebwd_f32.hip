@@ -1,0 +1,6 @@
+// Backward of the horizontal directions for large planes, fp32.
+#include "gspn_large_bwd_impl.hpp"
+
+namespace gspn {
+hipError_t large_bwd_h_f32(const LargeBwdHArgs& a) { return large_bwd_h_t<float>(a); }
+}  // namespace gspn

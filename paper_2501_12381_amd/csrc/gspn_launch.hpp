@@ -152,4 +152,31 @@ inline hipError_t large_fwd(const LargeFwdArgs& a) {
 }
 bool large_fwd_fits(int H, int W, int dtype);
 
+// backward of one horizontal direction for large planes (recompute + adjoint)
+struct LargeBwdHArgs {
+  const void* x;
+  const void* lam;
+  const void* dy;
+  const void* u;
+  const void* w;     // this direction's w0
+  void* dw;          // this direction's dw0
+  float* hbuf;       // B*C*H*W floats
+  float* hsum;
+  float* gsum;
+  float* state;      // large_bwd_state_floats(planes, H) floats
+  int first;         // first direction: hsum and gsum are stored, not added
+  int dir;           // 0: left-to-right, 1: right-to-left
+  int64_t planes;
+  int H, W;
+  int group;         // columns per local-GSPN group (0 or >= W: global)
+  void* stream;
+};
+
+inline int64_t large_bwd_state_floats(int64_t planes, int H) { return 6 * planes * (int64_t)H; }
+hipError_t large_bwd_h_f32(const LargeBwdHArgs& a);
+hipError_t large_bwd_h_bf16(const LargeBwdHArgs& a);
+inline hipError_t large_bwd_h(const LargeBwdHArgs& a, int dtype) {
+  return dtype == 0 ? large_bwd_h_f32(a) : large_bwd_h_bf16(a);
+}
+
 }  // namespace gspn

@@ -12,16 +12,17 @@ from tests.parity_util import assert_close, np64, oracle_bwd
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
-ALGOS = [L.GSPN_ALGO_AUTO, L.GSPN_ALGO_STREAM, L.GSPN_ALGO_RESIDENT, L.GSPN_ALGO_RESIDENT_GENERIC]
-ALGO_NAMES = {0: "auto", 1: "resident", 2: "stream", 3: "resident_generic"}
+ALGOS = [L.GSPN_ALGO_AUTO, L.GSPN_ALGO_STREAM, L.GSPN_ALGO_RESIDENT, L.GSPN_ALGO_RESIDENT_GENERIC,
+         L.GSPN_ALGO_TWO_PASS]
+ALGO_NAMES = {0: "auto", 1: "resident", 2: "stream", 3: "resident_generic", 4: "two_pass"}
 
 
 def run_bwd(inp, mask, algo):
     try:
         return ops.gspn_scan_bwd(inp["dy"], inp["x"], inp["w"], inp["lam"], inp["u"], mask, algo=algo)
     except L.GSPNError as e:
-        if e.status == 7 and algo in (L.GSPN_ALGO_RESIDENT, L.GSPN_ALGO_RESIDENT_GENERIC):
-            pytest.skip("resident kernel does not take this shape")
+        if e.status == 7 and algo in (L.GSPN_ALGO_RESIDENT, L.GSPN_ALGO_RESIDENT_GENERIC, L.GSPN_ALGO_TWO_PASS):
+            pytest.skip("this kernel family does not take this shape")
         raise
 
 

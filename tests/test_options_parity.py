@@ -17,7 +17,7 @@ pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
 ALGO_NAMES = {0: "auto", 1: "resident", 2: "stream", 3: "resident_generic", 4: "two_pass"}
 FWD_ALGOS = [0, 1, 2, 3, 4]
-BWD_ALGOS = [0, 1, 2, 3]
+BWD_ALGOS = [0, 1, 2, 3, 4]
 
 
 def inputs(B, C, H, W, mask, dtype, seed, lam_pd=False, u_pd=False, y_pd=False, logits=False):
