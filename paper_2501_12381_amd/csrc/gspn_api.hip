@@ -195,13 +195,18 @@ size_t fwd_ws_bytes(const Problem& p, int algo, uint32_t mask) {
   return 0;
 }
 
-// streaming and two-pass backward: h of one direction (the previous line's
-// for the streaming kernels), the running sums of h and g (fp32); the
-// two-pass kernels add the column state of their horizontal launches
+// streaming backward: the previous line's h of one direction, the running
+// sums of h and g (fp32 B*C*H*W arrays).  Two-pass backward: h of one
+// direction (a horizontal one, then top-to-bottom), the sums of the
+// horizontal directions' h and of every g, bottom-to-top's h when both
+// vertical directions are present, then the column state of the horizontal
+// launches.
+bool both_vertical(uint32_t mask) { return (mask & DIR_T2B) && (mask & DIR_B2T); }
 size_t bwd_ws_bytes(const Problem& p, int algo) {
-  if (algo == GSPN_ALGO_STREAM) return 3 * round_up((size_t)p.npc * 4, kWsAlign);
+  const size_t fb = round_up((size_t)p.npc * 4, kWsAlign);
+  if (algo == GSPN_ALGO_STREAM) return 3 * fb;
   if (algo == GSPN_ALGO_TWO_PASS)
-    return 3 * round_up((size_t)p.npc * 4, kWsAlign) +
+    return (both_vertical(p.mask) ? 4 : 3) * fb +
            round_up((size_t)gspn::large_bwd_state_floats(p.planes, (int)p.H) * 4, kWsAlign);
   return 0;
 }
@@ -374,28 +379,75 @@ int gspn_scan_bwd(const void* dy, const void* x, const void* w, const void* lam,
   float* hsum = (float*)((char*)workspace + fb);
   float* gsum = (float*)((char*)workspace + 2 * fb);
   const std::vector<int> ds = dirs_of(mask);
+  if (a == GSPN_ALGO_TWO_PASS) {
+    // horizontal directions first (their h through the first array), then the
+    // vertical directions' h at once (first and fourth arrays), then their
+    // adjoints; the finish adds the vertical h to the horizontal sum
+    float* hb = both_vertical(mask) ? (float*)((char*)workspace + 3 * fb) : nullptr;
+    float* state = (float*)((char*)workspace + (both_vertical(mask) ? 4 : 3) * fb);
+    int slot[4] = {-1, -1, -1, -1};
+    for (int i = 0; i < (int)ds.size(); ++i) slot[ds[i] == DIR_T2B ? 0 : ds[i] == DIR_B2T ? 1 : ds[i] == DIR_L2R ? 2 : 3] = i;
+    bool first = true;
+    for (int d = 2; d < 4; ++d) {
+      if (slot[d] < 0) continue;
+      LargeBwdHArgs l{};
+      l.x = x; l.lam = lam; l.dy = dy; l.u = u;
+      l.w = (const char*)w + (size_t)slot[d] * 3 * tb;
+      l.dw = (char*)dw + (size_t)slot[d] * 3 * tb;
+      l.hbuf = hprev; l.hsum = hsum; l.gsum = gsum; l.state = state;
+      l.first = first ? 1 : 0;
+      l.dir = d == 3 ? 1 : 0;
+      l.planes = p.planes; l.H = (int)H; l.W = (int)W;
+      l.group = p.gw;
+      l.stream = stream;
+      st = hip_status(large_bwd_h(l, dtype));
+      if (st != GSPN_OK) return st;
+      first = false;
+    }
+    float* hv[2] = {nullptr, nullptr};  // h of top-to-bottom, bottom-to-top
+    if (slot[0] >= 0 || slot[1] >= 0) {
+      hv[0] = slot[0] >= 0 ? hprev : nullptr;
+      hv[1] = slot[1] >= 0 ? (slot[0] >= 0 ? hb : hprev) : nullptr;
+      LargeBwdVArgs v{};
+      v.x = x; v.lam = lam; v.w = w;
+      v.slot_t2b = slot[0]; v.slot_b2t = slot[1];
+      v.h_t2b = hv[0]; v.h_b2t = hv[1];
+      v.planes = p.planes; v.H = (int)H; v.W = (int)W;
+      v.group = p.gh;
+      v.stream = stream;
+      st = hip_status(large_bwd_v_rec(v, dtype));
+      if (st != GSPN_OK) return st;
+    }
+    for (int d = 0; d < 2; ++d) {
+      if (slot[d] < 0) continue;
+      StreamAdjArgs r{};
+      r.dy = dy; r.u = u;
+      r.w = (const char*)w + (size_t)slot[d] * 3 * tb;
+      r.wstride = p.npc;
+      r.hprev = hv[d];
+      r.hshift = 1;
+      r.dw = (char*)dw + (size_t)slot[d] * 3 * tb;
+      r.gsum = gsum;
+      r.first = 0;
+      r.planes = p.planes; r.H = (int)H; r.W = (int)W; r.dir = d == 0 ? DIR_T2B : DIR_B2T; r.dtype = dtype;
+      r.group = p.gh;
+      r.stream = stream;
+      st = hip_status(stream_adj_pass(r));
+      if (st != GSPN_OK) return st;
+    }
+    GradFinishArgs g{};
+    g.x = x; g.lam = lam; g.dy = dy; g.gsum = gsum; g.hsum = hsum; g.hsum2 = hv[0] ? hv[0] : hv[1];
+    g.hsum3 = hv[0] ? hv[1] : nullptr;
+    g.dx = dx; g.dlam = dlam; g.du = du; g.n = p.npc; g.dtype = dtype;
+    g.stream = stream;
+    return hip_status(grad_finish(g));
+  }
   const bool per_dir = p.lam_pd() || p.u_pd() || p.y_pd();
   for (int i = 0; i < (int)ds.size(); ++i) {
     const void* dy_i = (const char*)dy + (p.y_pd() ? i * tb : 0);
     const void* lam_i = (const char*)lam + (p.lam_pd() ? i * tb : 0);
     const void* u_i = (const char*)u + (p.u_pd() ? i * tb : 0);
     const int group = (ds[i] == DIR_T2B || ds[i] == DIR_B2T) ? p.gh : p.gw;
-    if (a == GSPN_ALGO_TWO_PASS && (ds[i] == DIR_L2R || ds[i] == DIR_R2L)) {
-      LargeBwdHArgs l{};
-      l.x = x; l.lam = lam; l.dy = dy; l.u = u;
-      l.w = (const char*)w + (size_t)i * 3 * tb;
-      l.dw = (char*)dw + (size_t)i * 3 * tb;
-      l.hbuf = hprev; l.hsum = hsum; l.gsum = gsum;
-      l.state = (float*)((char*)workspace + 3 * fb);
-      l.first = i == 0;
-      l.dir = ds[i] == DIR_R2L ? 1 : 0;
-      l.planes = p.planes; l.H = (int)H; l.W = (int)W;
-      l.group = group;
-      l.stream = stream;
-      st = hip_status(large_bwd_h(l, dtype));
-      if (st != GSPN_OK) return st;
-      continue;
-    }
     StreamFwdArgs f{};
     f.x = x; f.lam = lam_i; f.u = nullptr; f.y = nullptr;
     f.w = (const char*)w + (size_t)i * 3 * tb;

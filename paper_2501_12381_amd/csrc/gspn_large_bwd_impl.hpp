@@ -354,4 +354,28 @@ hipError_t large_bwd_h_t(const LargeBwdHArgs& a) {
   return hipSuccess;
 }
 
+template <typename T>
+hipError_t large_bwd_v_rec_t(const LargeBwdVArgs& a) {
+  if (!large_fwd_supported<T>(a.H, a.W)) return hipErrorInvalidValue;
+  const LargeGeom<T> g = large_geom<T>(a.H, a.W);
+  const bool both = a.slot_t2b >= 0 && a.slot_b2t >= 0;
+  LargeVParams v{};
+  v.x = a.x; v.lam = a.lam; v.w = a.w; v.u = nullptr; v.y = nullptr;
+  v.acc = a.slot_t2b >= 0 ? a.h_t2b : a.h_b2t;
+  v.acc_b = both ? a.h_b2t : nullptr;
+  v.planes = a.planes; v.npc = a.planes * (int64_t)a.H * a.W; v.H = a.H; v.W = a.W;
+  v.slot0 = a.slot_t2b; v.slot1 = a.slot_b2t;
+  v.final_out = 0;
+  v.split = both ? 1 : 0;
+  v.grp = (a.group > 0 && a.group < a.H) ? a.group : a.H;
+  if (both && 2 * a.planes > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+  hipStream_t st = (hipStream_t)a.stream;
+  switch (g.wpd) {
+    case 1: return launch_large_v<T, 1>(v, false, st);
+    case 2: return launch_large_v<T, 2>(v, false, st);
+    case 4: return launch_large_v<T, 4>(v, false, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 }  // namespace gspn

@@ -56,6 +56,7 @@ struct StreamAdjArgs {
   int group;
   int logits, renorm;
   int lamw;           // per-direction lam: gsum accumulates lam * g, dlam written here
+  int hshift;         // hprev holds h itself: read one line back (zero at a group start)
   void* stream;
 };
 hipError_t stream_adj_pass_f32(const StreamAdjArgs& a);
@@ -70,6 +71,8 @@ struct GradFinishArgs {
   const void* dy;
   const float* gsum;
   const float* hsum;
+  const float* hsum2;  // further parts of sum_d h_d (null when absent)
+  const float* hsum3;
   void* dx;
   void* dlam;         // null when dlam was written per direction
   void* du;
@@ -173,6 +176,26 @@ struct LargeBwdHArgs {
 };
 
 inline int64_t large_bwd_state_floats(int64_t planes, int H) { return 6 * planes * (int64_t)H; }
+// recompute of the vertical directions' h for the same backward (the forward's
+// vertical pass storing h): top-to-bottom into h_t2b, bottom-to-top into
+// h_b2t (both present: one workgroup per direction and plane)
+struct LargeBwdVArgs {
+  const void* x;
+  const void* lam;
+  const void* w;     // all n directions, packed
+  int slot_t2b, slot_b2t;  // weight slots, -1 when absent
+  float* h_t2b;
+  float* h_b2t;
+  int64_t planes;
+  int H, W;
+  int group;         // rows per local-GSPN group (0: global)
+  void* stream;
+};
+hipError_t large_bwd_v_rec_f32(const LargeBwdVArgs& a);
+hipError_t large_bwd_v_rec_bf16(const LargeBwdVArgs& a);
+inline hipError_t large_bwd_v_rec(const LargeBwdVArgs& a, int dtype) {
+  return dtype == 0 ? large_bwd_v_rec_f32(a) : large_bwd_v_rec_bf16(a);
+}
 hipError_t large_bwd_h_f32(const LargeBwdHArgs& a);
 hipError_t large_bwd_h_bf16(const LargeBwdHArgs& a);
 inline hipError_t large_bwd_h(const LargeBwdHArgs& a, int dtype) {

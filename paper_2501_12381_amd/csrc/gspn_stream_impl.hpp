@@ -36,7 +36,7 @@ __device__ __forceinline__ void load_tile(const T* __restrict__ base, const Geo&
 #pragma unroll
     for (int l = 0; l < NL; ++l) {
       const int line = l0 + l;
-      if (line < g.L) {
+      if (line >= 0 && line < g.L) {
         const T* row = base + (int64_t)line * g.W;
         if (vec_ok && p0 + NP <= g.P) {
           ldv<NP>(row + p0, t[l]);
@@ -56,11 +56,11 @@ __device__ __forceinline__ void load_tile(const T* __restrict__ base, const Geo&
       float v[NL];
       if (pos < g.P) {
         const T* row = base + (int64_t)pos * g.W;
-        if (vec_ok && l0 + NL <= g.L) {
+        if (vec_ok && l0 >= 0 && l0 + NL <= g.L) {
           ldv<NL>(row + l0, v);
         } else {
 #pragma unroll
-          for (int l = 0; l < NL; ++l) v[l] = (l0 + l < g.L) ? to_f(row[l0 + l]) : 0.f;
+          for (int l = 0; l < NL; ++l) v[l] = (l0 + l >= 0 && l0 + l < g.L) ? to_f(row[l0 + l]) : 0.f;
         }
       } else {
 #pragma unroll
@@ -301,6 +301,8 @@ __global__ void __launch_bounds__(1024) stream_fwd_kernel(StreamFwdParams p) {
 // where gn, wn_k are g and w of the line after this one in scan order (none
 // when that line starts a group).
 //   dw_k[line][p] = g[p] * hprev[line][p + k - 1]   (logits: through Eq. 6's Jacobian)
+// hshift: hprev holds h itself (line by line), read one line back in scan
+// order, zero where a line starts a group
 //   gsum (+)= g   (lamw: gsum (+)= lam * g and dlam = x * g)
 // ---------------------------------------------------------------------------
 struct StreamAdjParams {
@@ -319,6 +321,7 @@ struct StreamAdjParams {
   int vec_ok, vec_ok_f;
   int G;
   int logits, renorm, lamw;
+  int hshift;
 };
 
 template <typename T, bool HZ, bool REV, int NP, int NL, bool EXT>
@@ -357,7 +360,7 @@ __global__ void __launch_bounds__(1024) stream_adj_kernel(StreamAdjParams p) {
     load_tile<HZ, NL, NP>(w, g, l0, p0, vec_ok, t0);
     load_tile<HZ, NL, NP>(w + wstride, g, l0, p0, vec_ok, t1);
     load_tile<HZ, NL, NP>(w + 2 * wstride, g, l0, p0, vec_ok, t2);
-    load_tile<HZ, NL, NP>(hprev, g, l0, p0, vec_ok_f, th);
+    load_tile<HZ, NL, NP>(hprev, g, p.hshift ? (REV ? l0 + 1 : l0 - 1) : l0, p0, vec_ok_f, th);
     if (!p.first) load_tile<HZ, NL, NP>(gsum, g, l0, p0, vec_ok_f, tg);
     else {
 #pragma unroll
@@ -377,6 +380,10 @@ __global__ void __launch_bounds__(1024) stream_adj_kernel(StreamAdjParams p) {
       const int l = adj_rev ? NL - 1 - ll : ll;
       const int line = l0 + l;
       if (line < g.L) {
+        if (p.hshift && group_start(line, p.G, REV)) {
+#pragma unroll
+          for (int q = 0; q < NP; ++q) th[l][q] = 0.f;
+        }
         // the line after this one (in scan order) starts a group: it took nothing from here
         const int nxt = REV ? line - 1 : line + 1;
         if (nxt >= 0 && nxt < g.L && group_start(nxt, p.G, REV)) {
@@ -450,23 +457,54 @@ __global__ void __launch_bounds__(1024) stream_adj_kernel(StreamAdjParams p) {
 
 // dx = lam * gsum (or gsum itself when it already holds sum_d lam_d g_d),
 // dlam = x * gsum (unless written per direction), du = dy * hsum, hsum, or
-// nothing (per-direction du)   (flat, elementwise)
-template <typename T>
+// nothing (per-direction du), where hsum may come in up to three fp32 arrays
+// (added in a fixed order).  Flat and elementwise; VEC: 8 elements a thread
+// with 16-byte accesses (every pointer 16-byte aligned, n a multiple of 8).
+template <typename T, int VEC>
 __global__ void __launch_bounds__(256)
 grad_finish_kernel(const T* __restrict__ x, const T* __restrict__ lam, const T* __restrict__ dy,
                    const float* __restrict__ gsum, const float* __restrict__ hsum,
+                   const float* __restrict__ hsum2, const float* __restrict__ hsum3,
                    T* __restrict__ dx, T* __restrict__ dlam, T* __restrict__ du, int64_t n,
                    int dx_mode, int du_mode) {
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
-    const float gs = gsum[i];
-    dx[i] = from_f<T>(dx_mode == 0 ? to_f(lam[i]) * gs : gs);
-    if (dlam) dlam[i] = from_f<T>(to_f(x[i]) * gs);
-    if (du_mode == 0) du[i] = from_f<T>(to_f(dy[i]) * hsum[i]);
-    else if (du_mode == 1) du[i] = from_f<T>(hsum[i]);
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x * VEC;
+  for (int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * VEC; i < n; i += stride) {
+    float gs[VEC], hs[VEC], a[VEC], o[VEC];
+    ldv<VEC>(gsum + i, gs);
+    if (dx_mode == 0) {
+      ldv<VEC>(lam + i, a);
+#pragma unroll
+      for (int q = 0; q < VEC; ++q) o[q] = a[q] * gs[q];
+      stv<VEC>(dx + i, o);
+    } else {
+      stv<VEC>(dx + i, gs);
+    }
+    if (dlam) {
+      ldv<VEC>(x + i, a);
+#pragma unroll
+      for (int q = 0; q < VEC; ++q) o[q] = a[q] * gs[q];
+      stv<VEC>(dlam + i, o);
+    }
+    if (du_mode == 2) continue;
+    ldv<VEC>(hsum + i, hs);
+    if (hsum2) {
+      ldv<VEC>(hsum2 + i, a);
+#pragma unroll
+      for (int q = 0; q < VEC; ++q) hs[q] += a[q];
+    }
+    if (hsum3) {
+      ldv<VEC>(hsum3 + i, a);
+#pragma unroll
+      for (int q = 0; q < VEC; ++q) hs[q] += a[q];
+    }
+    if (du_mode == 0) {
+      ldv<VEC>(dy + i, a);
+#pragma unroll
+      for (int q = 0; q < VEC; ++q) hs[q] *= a[q];
+    }
+    stv<VEC>(du + i, hs);
   }
 }
-
 
 // ---------------------------------------------------------------------------
 // host-side launchers, instantiated once per element type
@@ -578,6 +616,7 @@ hipError_t adj_dir(const StreamAdjArgs& a, const Geo& g) {
   p.vec_ok_f = vec_ok_for(HZ, s.np, 8 / s.np, g.W, fp, 2, sizeof(float));
   p.G = (a.group <= 0 || a.group >= g.L) ? g.L : a.group;
   p.logits = a.logits; p.renorm = a.renorm; p.lamw = a.lamw;
+  p.hshift = a.hshift;
   const bool ext = a.logits || a.lamw;
   hipStream_t st = (hipStream_t)a.stream;
   switch (s.np) {
@@ -619,11 +658,19 @@ hipError_t stream_adj_pass_t(const StreamAdjArgs& a) {
 template <typename T>
 hipError_t grad_finish_t(const GradFinishArgs& a) {
   const int64_t n = a.n;
-  int64_t blocks = (n + 255) / 256;
+  bool vec = n % 8 == 0;
+  for (const void* q : {(const void*)a.x, (const void*)a.lam, (const void*)a.dy, (const void*)a.gsum,
+                        (const void*)a.hsum, (const void*)a.hsum2, (const void*)a.hsum3, (const void*)a.dx,
+                        (const void*)a.dlam, (const void*)a.du})
+    if ((uintptr_t)q % 16) vec = false;
+  const int per = vec ? 8 : 1;
+  int64_t blocks = (n / per + 255) / 256;
   if (blocks > 65536) blocks = 65536;
-  hipLaunchKernelGGL(grad_finish_kernel<T>, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)a.stream,
-                     (const T*)a.x, (const T*)a.lam, (const T*)a.dy, a.gsum, a.hsum, (T*)a.dx,
-                     (T*)a.dlam, (T*)a.du, n, a.dx_mode, a.du_mode);
+  if (blocks < 1) blocks = 1;
+  auto kern = vec ? grad_finish_kernel<T, 8> : grad_finish_kernel<T, 1>;
+  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)a.stream,
+                     (const T*)a.x, (const T*)a.lam, (const T*)a.dy, a.gsum, a.hsum, a.hsum2, a.hsum3,
+                     (T*)a.dx, (T*)a.dlam, (T*)a.du, n, a.dx_mode, a.du_mode);
   return hipGetLastError();
 }
 

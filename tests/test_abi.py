@@ -86,14 +86,16 @@ def test_workspace_sizes():
     assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 56, 0xF, bf, algo=T) == 0  # row under 128 bytes
     assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 32, 0xF, f32, algo=T) == 2 * (2 * 3 * 5 * 32 * 4) + 512
     # two-pass backward (a horizontal direction present): h of one direction,
-    # the sums of h and g (fp32 each), then the column state of its horizontal
-    # launches (2 parities x 3 products x planes x H floats: 720 B -> 768)
-    assert L.gspn_scan_bwd_workspace_bytes(2, 3, 5, 64, 0xF, bf, algo=T) == 3 * acc + 768
+    # the sum of the horizontal h, the sum of g (fp32 each), bottom-to-top's h
+    # when both vertical directions are present, then the column state of the
+    # horizontal launches (2 parities x 3 products x planes x H floats: 720 B -> 768)
+    assert L.gspn_scan_bwd_workspace_bytes(2, 3, 5, 64, 0xF, bf, algo=T) == 4 * acc + 768
     assert L.gspn_scan_bwd_workspace_bytes(2, 3, 5, 64, 0x4, bf, algo=T) == 3 * acc + 768
+    assert L.gspn_scan_bwd_workspace_bytes(2, 3, 5, 64, 0x5, bf, algo=T) == 3 * acc + 768
     assert L.gspn_scan_bwd_workspace_bytes(2, 3, 5, 64, 0x3, bf, algo=T) == 0  # no horizontal direction
     assert L.gspn_scan_bwd_workspace_bytes(2, 3, 5, 60, 0xF, bf, algo=T) == 0
     big_b = L.gspn_scan_bwd_workspace_bytes(1, 2, 2048, 2048, 0xF, bf, algo=L.GSPN_ALGO_AUTO)
-    assert big_b == 3 * (2 * 2048 * 2048 * 4) + 6 * 2 * 2048 * 4
+    assert big_b == 4 * (2 * 2048 * 2048 * 4) + 6 * 2 * 2048 * 4
     # AUTO takes the two-pass kernels for planes that do not fit on chip
     big = L.gspn_scan_fwd_workspace_bytes(1, 2, 2048, 2048, 0xF, bf, algo=L.GSPN_ALGO_AUTO)
     assert big == 2 * (2 * 2048 * 2048 * 4) + 4 * 2 * 2048 * 4
