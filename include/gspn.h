@@ -129,8 +129,10 @@ enum {
                             otherwise).  Backward (a horizontal direction in the
                             mask): each horizontal direction recomputes its h into
                             the workspace block by block, then runs the adjoint over
-                            the blocks in reverse order; vertical directions stream.
-                            Workspace: three fp32 B*C*H*W arrays and 6*B*C*H floats.
+                            the blocks in reverse order; the vertical directions
+                            recompute their h in one pass and run both adjoints in
+                            another.  Workspace: three fp32 B*C*H*W arrays (four
+                            with both vertical directions) and 6*B*C*H floats.
                             Needs W * element size a multiple of 16 bytes and at
                             least 128 bytes, W <= 4096 (bf16) or 2048 (f32), and
                             16-byte aligned tensors (AUTO falls back to streaming). */

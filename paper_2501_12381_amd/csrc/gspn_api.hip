@@ -418,21 +418,16 @@ int gspn_scan_bwd(const void* dy, const void* x, const void* w, const void* lam,
       st = hip_status(large_bwd_v_rec(v, dtype));
       if (st != GSPN_OK) return st;
     }
-    for (int d = 0; d < 2; ++d) {
-      if (slot[d] < 0) continue;
-      StreamAdjArgs r{};
-      r.dy = dy; r.u = u;
-      r.w = (const char*)w + (size_t)slot[d] * 3 * tb;
-      r.wstride = p.npc;
-      r.hprev = hv[d];
-      r.hshift = 1;
-      r.dw = (char*)dw + (size_t)slot[d] * 3 * tb;
+    if (slot[0] >= 0 || slot[1] >= 0) {
+      LargeBwdVAdjArgs r{};
+      r.dy = dy; r.u = u; r.w = w; r.dw = dw;
+      r.slot_t2b = slot[0]; r.slot_b2t = slot[1];
+      r.h_t2b = hv[0]; r.h_b2t = hv[1];
       r.gsum = gsum;
-      r.first = 0;
-      r.planes = p.planes; r.H = (int)H; r.W = (int)W; r.dir = d == 0 ? DIR_T2B : DIR_B2T; r.dtype = dtype;
+      r.planes = p.planes; r.H = (int)H; r.W = (int)W;
       r.group = p.gh;
       r.stream = stream;
-      st = hip_status(stream_adj_pass(r));
+      st = hip_status(large_bwd_v_adj(r, dtype));
       if (st != GSPN_OK) return st;
     }
     GradFinishArgs g{};

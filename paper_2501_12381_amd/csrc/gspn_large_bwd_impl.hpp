@@ -1,14 +1,15 @@
-// Backward of the horizontal directions for planes too large to keep on chip
-// (e.g. 2048 x 2048): the exact adjoint of Eq. 1 along columns, one direction
-// at a time, in two launch sequences over blocks of K columns (K = 128 bytes
-// of a row, the block of the forward's pass H):
+// Two-pass backward for planes too large to keep on chip (e.g. 2048 x 2048):
+// the exact adjoint of Eq. 1-2 in launch sequences that each stream the plane
+// once, with fp32 h and g sums in the workspace.
 //
+// Horizontal directions, one at a time, over blocks of K columns (K = 128
+// bytes of a row, the block of the forward's pass H):
 //   recompute  large_h_kernel in its `rec` mode, blocks in scan order: h of
 //              the direction into an fp32 plane `hbuf`, and hsum (+)= h.
-//   adjoint    large_hadj_kernel below, blocks in reverse scan order.  A
-//              workgroup owns a band of rows plus a halo of K rows on each
-//              side (one row per lane), as in the forward: starting from the
-//              exact products of the column after the block (carried between
+//   adjoint    large_hadj_kernel, blocks in reverse scan order.  A workgroup
+//              owns a band of rows plus a halo of K rows on each side (one
+//              row per lane), as in the forward: starting from the exact
+//              products of the column after the block (carried between
 //              launches in a small workspace), the transposed stencil
 //                g[l][p] = u dy[l][p] + w0[n][p+1] g[n][p+1] + w1[n][p] g[n][p]
 //                          + w2[n][p-1] g[n][p-1]          (n: the next line)
@@ -17,11 +18,18 @@
 //                dw_k[l][p] = g[l][p] h[prev][p+k-1]
 //              is formed per step in registers and stored as 128-byte row
 //              segments; g replaces the h column that no later step reads and
-//              is added to gsum with coalesced accesses at the end.
-//
-// The row segments of dy, u and the three weight maps come in as one register
-// tile per launch, like the forward's; the dw words are produced as the tile
-// words die, so the two share the register budget.
+//              is added to gsum with coalesced accesses at the end.  The row
+//              segments of dy, u and the three weight maps come in as one
+//              register tile per launch; the dw words are produced as the tile
+//              words die, so the two share the register budget.
+// Vertical directions, both at once:
+//   recompute  the forward's vertical pass (one workgroup per direction and
+//              plane) storing each direction's h in its own fp32 plane.
+//   adjoint    large_vadj_kernel: one workgroup per plane, top-to-bottom's
+//              adjoint walking up and bottom-to-top's walking down, meeting at
+//              the middle row; rows stream through register rings.
+// The gradient finish then forms dx = lam gsum, dlam = x gsum and
+// du = dy (hsum + h_t2b + h_b2t).
 #pragma once
 
 #include "gspn_large_impl.hpp"
@@ -374,6 +382,305 @@ hipError_t large_bwd_v_rec_t(const LargeBwdVArgs& a) {
     case 1: return launch_large_v<T, 1>(v, false, st);
     case 2: return launch_large_v<T, 2>(v, false, st);
     case 4: return launch_large_v<T, 4>(v, false, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+
+// ---------------------------------------------------------------------------
+// adjoint of the vertical directions (after large_bwd_v_rec): one workgroup per
+// plane.  Top-to-bottom's adjoint walks the rows upwards, bottom-to-top's
+// downwards; with both present each takes half of the waves and they meet at
+// the middle row, as the forward's vertical pass does (every row's g is added
+// to gsum by the direction that reaches it first, then, after a barrier, by
+// the other).  Lanes hold chunk-interleaved positions (whole cache lines per
+// load instruction); rows stream through register rings.  Per row:
+//   g = u dy + [a1 + a0(p+1) + a2(p-1)]   (a_k = w_k g of the previous row done)
+//   dw_k = g h[prev](p+k-1),   gsum += g
+// ---------------------------------------------------------------------------
+struct LargeVAdjParams {
+  const void* dy;
+  const void* u;
+  const void* w;        // all directions, packed
+  void* dw;             // all directions, packed
+  const float* h[2];    // h of top-to-bottom, bottom-to-top
+  float* gsum;
+  int64_t planes, npc;
+  int H, W;
+  int slot[2];          // weight slots of top-to-bottom, bottom-to-top (-1 absent)
+  int grp;              // rows per local-GSPN group (H: global)
+};
+
+template <typename T, int WPD, bool BOTH>
+__global__ void __launch_bounds__((BOTH ? 128 : 64) * WPD, 2) large_vadj_kernel(LargeVAdjParams p) {
+  using C = LargeCfg<T>;
+  // rings: R rows of the bf16/fp32 input maps, RH rows of h, RA rows of gsum
+  constexpr int NP = C::NPV, R = C::RV, RH = 1, RA = 1;
+  constexpr int G = 4;            // positions per lane and chunk
+  constexpr int NQ = NP / G;      // chunks per wave span
+  constexpr int SPAN = 64 * G;    // positions per chunk
+  typedef Pack<T, G> PK;
+  __shared__ float edge[2][2 * WPD][2];  // [step parity][wave][a0 of the first position, a2 of the last]
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int dir = BOTH ? (wave >= WPD ? 1 : 0) : (p.slot[0] >= 0 ? 0 : 1);
+  const int wi = BOTH ? wave - dir * WPD : wave;
+  const int64_t plane = blockIdx.x;
+  const int H = p.H, W = p.W;
+  int po[NQ];
+  bool qok[NQ];
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    const int pos = wi * NQ * SPAN + q * SPAN + lane * G;
+    qok[q] = pos < W;  // W is a multiple of G
+    po[q] = qok[q] ? pos : 0;
+  }
+  const int wlo = wi * NQ * SPAN - 1, whi = (wi + 1) * NQ * SPAN;  // neighbours of the wave's span
+  const bool wlo_ok = wlo >= 0, whi_ok = whi < W;
+  const int64_t pb = plane * (int64_t)H * W;
+  const int slot = p.slot[dir];
+  const int odd = BOTH ? (H & 1) : 0;
+  const int nsteps = H + odd;
+  const int sm = BOTH ? H / 2 + odd : nsteps;  // first step of the second half
+  const int delay = dir ? odd : 0;
+  const int grp = p.grp;
+
+  for (int i = threadIdx.x; i < 2 * 2 * WPD * 2; i += blockDim.x) (&edge[0][0][0])[i] = 0.f;
+  __syncthreads();
+
+  const T* w0 = (const T*)p.w + (int64_t)slot * 3 * p.npc + pb;
+  const T* base[5] = {(const T*)p.dy + pb, (const T*)p.u + pb, w0, w0 + p.npc, w0 + 2 * p.npc};
+  T* d0 = (T*)p.dw + (int64_t)slot * 3 * p.npc + pb;
+  const float* hb = p.h[dir] + pb;
+  float* gs = p.gsum + pb;
+
+  auto t_of = [&](int s) { return s - delay; };
+  // adjoint order: top-to-bottom's rows upwards, bottom-to-top's downwards
+  auto line_of = [&](int t) {
+    t = t < 0 ? 0 : (t >= H ? H - 1 : t);
+    return dir ? t : H - 1 - t;
+  };
+  auto prev_of = [&](int line) { return dir ? line + 1 : line - 1; };  // previous row in scan order
+  // scan order enters a group at its first line (top-to-bottom: lowest row)
+  auto starts = [&](int line) { return dir ? ((line + 1) % grp == 0) : (line % grp == 0); };
+
+  PK ring[R][5][NQ];
+  float hring[RH][NQ][G];
+  float hedge[RH][2];
+  auto load_main = [&](int k, int s) __attribute__((always_inline)) {
+    const int64_t off = (int64_t)line_of(t_of(s)) * W;
+#pragma unroll
+    for (int m = 0; m < 5; ++m)
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) ring[k][m][q].load(base[m] + off + po[q]);
+  };
+  auto load_h = [&](int k, int s) __attribute__((always_inline)) {
+    int pl = prev_of(line_of(t_of(s)));
+    pl = pl < 0 ? 0 : (pl >= H ? H - 1 : pl);
+    const int64_t hoff = (int64_t)pl * W;
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) ldv<G>(hb + hoff + po[q], hring[k][q]);
+    hedge[k][0] = hb[hoff + (wlo_ok ? wlo : 0)];
+    hedge[k][1] = hb[hoff + (whi_ok ? whi : 0)];
+  };
+  float gring[RA][NQ][G];
+  auto load_aux = [&](int k, int s) __attribute__((always_inline)) {
+    const int64_t off = (int64_t)line_of(t_of(s)) * W;
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) ldv<G>(gs + off + po[q], gring[k][q]);
+  };
+  auto consume = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+#pragma unroll
+      for (int m = 0; m < 5; ++m)
+#pragma unroll
+        for (int q = 0; q < NQ; ++q)
+#pragma unroll
+          for (int i = 0; i < PK::kWords; ++i) asm volatile("" ::"v"(ring[k][m][q].w[i]));
+    }
+#pragma unroll
+    for (int k = 0; k < RH; ++k) {
+#pragma unroll
+      for (int q = 0; q < NQ; ++q)
+#pragma unroll
+        for (int j = 0; j < G; ++j) asm volatile("" ::"v"(hring[k][q][j]));
+      asm volatile("" ::"v"(hedge[k][0]), "v"(hedge[k][1]));
+    }
+#pragma unroll
+    for (int k = 0; k < RA; ++k)
+#pragma unroll
+      for (int q = 0; q < NQ; ++q)
+#pragma unroll
+        for (int j = 0; j < G; ++j) asm volatile("" ::"v"(gring[k][q][j]));
+  };
+
+  float a0[NQ][G], a1[NQ][G], a2[NQ][G];  // w_k * g of the previous row done
+#pragma unroll
+  for (int q = 0; q < NQ; ++q)
+#pragma unroll
+    for (int j = 0; j < G; ++j) a0[q][j] = a1[q][j] = a2[q][j] = 0.f;
+
+  // one step; the gsum refills stop at s_end (the middle, before the barrier)
+  auto step = [&](int k, int s, int s_end) __attribute__((always_inline)) {
+    const int t = t_of(s);
+    const bool act = t >= 0 && t < H;
+    const int par = s & 1;
+    const int line = line_of(t);
+    const int nx = dir ? line - 1 : line + 1;  // next row in scan order
+    const bool zr = !(nx >= 0 && nx < H) || starts(nx);
+    const int pl = prev_of(line);
+    const bool hzero = !(pl >= 0 && pl < H) || starts(line);  // no previous state
+    // a0 from position p+1 and a2 from p-1 (previous row done), across lanes,
+    // chunks and waves
+    float ar[NQ], al[NQ];
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      ar[q] = from_next_lane(a0[q][0]);
+      al[q] = from_prev_lane(a2[q][G - 1]);
+    }
+    float er = 0.f, el = 0.f;
+    if constexpr (WPD > 1) {
+      const float nr = edge[par ^ 1][wi < WPD - 1 ? wave + 1 : wave][0];
+      const float nl = edge[par ^ 1][wi > 0 ? wave - 1 : wave][1];
+      er = wi < WPD - 1 ? nr : 0.f;
+      el = wi > 0 ? nl : 0.f;
+    }
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const float cr = q < NQ - 1 ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(
+                                                              __builtin_bit_cast(int, a0[q + 1][0]), 0))
+                                  : er;
+      const float cl = q > 0 ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(
+                                                         __builtin_bit_cast(int, a2[q - 1][G - 1]), 63))
+                             : el;
+      if (lane == 63) ar[q] = cr;
+      if (lane == 0) al[q] = cl;
+    }
+    // h of the previous row and its neighbours (zero past the row end)
+    const float(&hv)[NQ][G] = hring[k % RH];
+    float hr[NQ], hl[NQ], hf[NQ], hb3[NQ];
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      hf[q] = qok[q] ? hv[q][0] : 0.f;
+      hb3[q] = qok[q] ? hv[q][G - 1] : 0.f;
+      hr[q] = from_next_lane(hf[q]);
+      hl[q] = from_prev_lane(hb3[q]);
+    }
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const float n0 = q < NQ - 1 ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, hf[q + 1]), 0))
+                                  : (whi_ok ? hedge[k % RH][1] : 0.f);
+      const float n3 = q > 0 ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, hb3[q - 1]), 63))
+                             : (wlo_ok ? hedge[k % RH][0] : 0.f);
+      if (lane == 63) hr[q] = n0;
+      if (lane == 0) hl[q] = n3;
+    }
+    // chunk by chunk: g from the old products, then the new products, dw and
+    // gsum stored at once (keeps few values live)
+    const int64_t off = (int64_t)line * W;
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const bool ok = qok[q] && act;
+      const PK(&v)[5][NQ] = ring[k];
+      float g[G];
+#pragma unroll
+      for (int j = 0; j < G; ++j) {
+        const float an = j == G - 1 ? ar[q] : a0[q][j + 1];
+        const float ap = j == 0 ? al[q] : a2[q][j - 1];
+        const float in = zr ? 0.f : a1[q][j] + an + ap;
+        const float gv = fmaf(v[1][q].get(j), v[0][q].get(j), in);
+        g[j] = ok ? gv : 0.f;
+      }
+      float dv[3][G], go[G];
+#pragma unroll
+      for (int j = 0; j < G; ++j) {
+        a0[q][j] = v[2][q].get(j) * g[j];
+        a1[q][j] = v[3][q].get(j) * g[j];
+        a2[q][j] = v[4][q].get(j) * g[j];
+        const float hm = hzero ? 0.f : hv[q][j];
+        const float hlv = hzero ? 0.f : (j == 0 ? hl[q] : hv[q][j - 1]);
+        const float hrv = hzero ? 0.f : (j == G - 1 ? hr[q] : hv[q][j + 1]);
+        dv[0][j] = g[j] * hlv;
+        dv[1][j] = g[j] * hm;
+        dv[2][j] = g[j] * hrv;
+        go[j] = gring[k % RA][q][j] + g[j];
+      }
+      if (ok) {
+#pragma unroll
+        for (int m = 0; m < 3; ++m) stv<G>(d0 + (int64_t)m * p.npc + off + po[q], dv[m]);
+        stv<G>(gs + off + po[q], go);
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < NQ; ++q)
+#pragma unroll
+      for (int j = 0; j < G; ++j) {
+        asm volatile("" : "+v"(a0[q][j]));
+        asm volatile("" : "+v"(a1[q][j]));
+        asm volatile("" : "+v"(a2[q][j]));
+      }
+    if (lane == 0) edge[par][wave][0] = a0[0][0];
+    if (lane == 63) edge[par][wave][1] = a2[NQ - 1][G - 1];
+    asm volatile("" ::: "memory");
+    load_main(k, s + R);
+    load_h(k % RH, s + RH);
+    if (s + RA < s_end) load_aux(k % RA, s + RA);
+    lds_barrier();
+  };
+
+  // first half: rows this direction reaches first; second half (after every
+  // wave's first-half gsum stores are visible): the rest
+  const int o = (R - sm % R) % R;  // idle steps before step 0 align the first loop to the ring
+  static_assert(R % RA == 0 && R % RH == 0, "the small rings' slots repeat with the main ring");
+#pragma unroll
+  for (int k = 0; k < R; ++k) load_main(k, k - o);
+#pragma unroll
+  for (int k = 0; k < RH; ++k) load_h(k, k - o);
+#pragma unroll
+  for (int k = 0; k < RA; ++k) load_aux(k, k - o);
+  for (int s0 = -o; s0 < sm; s0 += R) {
+#pragma unroll
+    for (int k = 0; k < R; ++k) step(k, s0 + k, sm);
+  }
+  if (sm < nsteps) {
+    consume();
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < RA; ++k) load_aux(k, sm + k);
+    for (int s0 = sm; s0 < nsteps; s0 += R) {
+#pragma unroll
+      for (int k = 0; k < R; ++k) step(k, s0 + k, nsteps + R);
+    }
+  }
+  consume();
+}
+
+template <typename T, int WPD, bool BOTH>
+hipError_t launch_large_vadj_mode(const LargeVAdjParams& p, hipStream_t st) {
+  hipLaunchKernelGGL((large_vadj_kernel<T, WPD, BOTH>), dim3((unsigned)p.planes), dim3((BOTH ? 128 : 64) * WPD),
+                     0, st, p);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t large_bwd_v_adj_t(const LargeBwdVAdjArgs& a) {
+  if (!large_fwd_supported<T>(a.H, a.W)) return hipErrorInvalidValue;
+  if (a.planes > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+  const LargeGeom<T> g = large_geom<T>(a.H, a.W);
+  LargeVAdjParams p{};
+  p.dy = a.dy; p.u = a.u; p.w = a.w; p.dw = a.dw;
+  p.h[0] = a.h_t2b; p.h[1] = a.h_b2t;
+  p.gsum = a.gsum;
+  p.planes = a.planes; p.npc = a.planes * (int64_t)a.H * a.W; p.H = a.H; p.W = a.W;
+  p.slot[0] = a.slot_t2b; p.slot[1] = a.slot_b2t;
+  p.grp = (a.group > 0 && a.group < a.H) ? a.group : a.H;
+  const bool both = a.slot_t2b >= 0 && a.slot_b2t >= 0;
+  hipStream_t st = (hipStream_t)a.stream;
+  switch (g.wpd) {
+    case 1: return both ? launch_large_vadj_mode<T, 1, true>(p, st) : launch_large_vadj_mode<T, 1, false>(p, st);
+    case 2: return both ? launch_large_vadj_mode<T, 2, true>(p, st) : launch_large_vadj_mode<T, 2, false>(p, st);
+    case 4: return both ? launch_large_vadj_mode<T, 4, true>(p, st) : launch_large_vadj_mode<T, 4, false>(p, st);
     default: return hipErrorInvalidValue;
   }
 }

@@ -56,7 +56,6 @@ struct StreamAdjArgs {
   int group;
   int logits, renorm;
   int lamw;           // per-direction lam: gsum accumulates lam * g, dlam written here
-  int hshift;         // hprev holds h itself: read one line back (zero at a group start)
   void* stream;
 };
 hipError_t stream_adj_pass_f32(const StreamAdjArgs& a);
@@ -195,6 +194,27 @@ hipError_t large_bwd_v_rec_f32(const LargeBwdVArgs& a);
 hipError_t large_bwd_v_rec_bf16(const LargeBwdVArgs& a);
 inline hipError_t large_bwd_v_rec(const LargeBwdVArgs& a, int dtype) {
   return dtype == 0 ? large_bwd_v_rec_f32(a) : large_bwd_v_rec_bf16(a);
+}
+// adjoint of the vertical directions for the same backward (after
+// large_bwd_v_rec): dw of both, gsum += g (fixed order)
+struct LargeBwdVAdjArgs {
+  const void* dy;
+  const void* u;
+  const void* w;     // all n directions, packed
+  void* dw;          // all n directions, packed
+  int slot_t2b, slot_b2t;
+  const float* h_t2b;
+  const float* h_b2t;
+  float* gsum;
+  int64_t planes;
+  int H, W;
+  int group;
+  void* stream;
+};
+hipError_t large_bwd_v_adj_f32(const LargeBwdVAdjArgs& a);
+hipError_t large_bwd_v_adj_bf16(const LargeBwdVAdjArgs& a);
+inline hipError_t large_bwd_v_adj(const LargeBwdVAdjArgs& a, int dtype) {
+  return dtype == 0 ? large_bwd_v_adj_f32(a) : large_bwd_v_adj_bf16(a);
 }
 hipError_t large_bwd_h_f32(const LargeBwdHArgs& a);
 hipError_t large_bwd_h_bf16(const LargeBwdHArgs& a);

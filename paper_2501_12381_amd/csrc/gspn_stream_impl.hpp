@@ -301,8 +301,6 @@ __global__ void __launch_bounds__(1024) stream_fwd_kernel(StreamFwdParams p) {
 // where gn, wn_k are g and w of the line after this one in scan order (none
 // when that line starts a group).
 //   dw_k[line][p] = g[p] * hprev[line][p + k - 1]   (logits: through Eq. 6's Jacobian)
-// hshift: hprev holds h itself (line by line), read one line back in scan
-// order, zero where a line starts a group
 //   gsum (+)= g   (lamw: gsum (+)= lam * g and dlam = x * g)
 // ---------------------------------------------------------------------------
 struct StreamAdjParams {
@@ -321,7 +319,6 @@ struct StreamAdjParams {
   int vec_ok, vec_ok_f;
   int G;
   int logits, renorm, lamw;
-  int hshift;
 };
 
 template <typename T, bool HZ, bool REV, int NP, int NL, bool EXT>
@@ -360,7 +357,7 @@ __global__ void __launch_bounds__(1024) stream_adj_kernel(StreamAdjParams p) {
     load_tile<HZ, NL, NP>(w, g, l0, p0, vec_ok, t0);
     load_tile<HZ, NL, NP>(w + wstride, g, l0, p0, vec_ok, t1);
     load_tile<HZ, NL, NP>(w + 2 * wstride, g, l0, p0, vec_ok, t2);
-    load_tile<HZ, NL, NP>(hprev, g, p.hshift ? (REV ? l0 + 1 : l0 - 1) : l0, p0, vec_ok_f, th);
+    load_tile<HZ, NL, NP>(hprev, g, l0, p0, vec_ok_f, th);
     if (!p.first) load_tile<HZ, NL, NP>(gsum, g, l0, p0, vec_ok_f, tg);
     else {
 #pragma unroll
@@ -380,10 +377,6 @@ __global__ void __launch_bounds__(1024) stream_adj_kernel(StreamAdjParams p) {
       const int l = adj_rev ? NL - 1 - ll : ll;
       const int line = l0 + l;
       if (line < g.L) {
-        if (p.hshift && group_start(line, p.G, REV)) {
-#pragma unroll
-          for (int q = 0; q < NP; ++q) th[l][q] = 0.f;
-        }
         // the line after this one (in scan order) starts a group: it took nothing from here
         const int nxt = REV ? line - 1 : line + 1;
         if (nxt >= 0 && nxt < g.L && group_start(nxt, p.G, REV)) {
@@ -616,7 +609,6 @@ hipError_t adj_dir(const StreamAdjArgs& a, const Geo& g) {
   p.vec_ok_f = vec_ok_for(HZ, s.np, 8 / s.np, g.W, fp, 2, sizeof(float));
   p.G = (a.group <= 0 || a.group >= g.L) ? g.L : a.group;
   p.logits = a.logits; p.renorm = a.renorm; p.lamw = a.lamw;
-  p.hshift = a.hshift;
   const bool ext = a.logits || a.lamw;
   hipStream_t st = (hipStream_t)a.stream;
   switch (s.np) {
