@@ -4,7 +4,7 @@
 //
 // Horizontal directions, one at a time, over blocks of K columns (K = 128
 // bytes of a row, the block of the forward's pass H):
-//   recompute  large_h_kernel in its `rec` mode, blocks in scan order: h of
+//   recompute  large_hrec_kernel (pass H in its `rec` mode), blocks in scan order: h of
 //              the direction into an fp32 plane `hbuf`, and hsum (+)= h.
 //   adjoint    large_hadj_kernel, blocks in reverse scan order.  A workgroup
 //              owns a band of rows plus a halo of K rows on each side (one
@@ -23,8 +23,9 @@
 //              register tile per launch; the dw words are produced as the tile
 //              words die, so the two share the register budget.
 // Vertical directions, both at once:
-//   recompute  the forward's vertical pass (one workgroup per direction and
-//              plane) storing each direction's h in its own fp32 plane.
+//   recompute  large_vrec_kernel, the forward's vertical pass (one workgroup
+//              per direction and plane) storing each direction's h in its own
+//              fp32 plane.
 //   adjoint    large_vadj_kernel: one workgroup per plane, top-to-bottom's
 //              adjoint walking up and bottom-to-top's walking down, meeting at
 //              the middle row; rows stream through register rings.
@@ -379,9 +380,9 @@ hipError_t large_bwd_v_rec_t(const LargeBwdVArgs& a) {
   if (both && 2 * a.planes > 0x7fffffffLL) return hipErrorInvalidConfiguration;
   hipStream_t st = (hipStream_t)a.stream;
   switch (g.wpd) {
-    case 1: return launch_large_v<T, 1>(v, false, st);
-    case 2: return launch_large_v<T, 2>(v, false, st);
-    case 4: return launch_large_v<T, 4>(v, false, st);
+    case 1: return launch_large_v<T, 1>(v, false, st, true);
+    case 2: return launch_large_v<T, 2>(v, false, st, true);
+    case 4: return launch_large_v<T, 4>(v, false, st, true);
     default: return hipErrorInvalidValue;
   }
 }

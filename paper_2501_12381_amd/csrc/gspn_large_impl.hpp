@@ -75,7 +75,7 @@ struct LargeVParams {
 //
 // BOTH: both vertical directions are present; FIN: write y (no pass H follows).
 template <typename T, int WPD, bool BOTH, bool FIN>
-__global__ void __launch_bounds__(128 * WPD, 2) large_v_kernel(LargeVParams p) {
+__device__ __forceinline__ void large_v_body(const LargeVParams& p) {
   using C = LargeCfg<T>;
   constexpr int NP = C::NPV, R = C::RV, RA = C::RA;
   static_assert(R % RA == 0, "acc ring slots must repeat with the input ring");
@@ -304,6 +304,17 @@ __global__ void __launch_bounds__(128 * WPD, 2) large_v_kernel(LargeVParams p) {
     }
 }
 
+template <typename T, int WPD, bool BOTH, bool FIN>
+__global__ void __launch_bounds__(128 * WPD, 2) large_v_kernel(LargeVParams p) {
+  large_v_body<T, WPD, BOTH, FIN>(p);
+}
+// the same pass as the backward's recompute of the vertical directions' h
+// (its own name in kernel traces and counter profiles)
+template <typename T, int WPD, bool BOTH, bool FIN>
+__global__ void __launch_bounds__(128 * WPD, 2) large_vrec_kernel(LargeVParams p) {
+  large_v_body<T, WPD, BOTH, FIN>(p);
+}
+
 // ---------------------------------------------------------------------------
 // pass H
 // ---------------------------------------------------------------------------
@@ -335,7 +346,7 @@ struct LargeHParams {
 };
 
 template <typename T, int NW>
-__global__ void __launch_bounds__(64 * NW) large_h_kernel(LargeHParams p) {
+__device__ __forceinline__ void large_h_body(const LargeHParams& p) {
   using C = LargeCfg<T>;
   constexpr int K = C::KH, HV = C::HV, VE = C::VE, KP = K + 1;
   typedef Pack<T, VE> PK;
@@ -516,6 +527,17 @@ __global__ void __launch_bounds__(64 * NW) large_h_kernel(LargeHParams p) {
   }
 }
 
+template <typename T, int NW>
+__global__ void __launch_bounds__(64 * NW) large_h_kernel(LargeHParams p) {
+  large_h_body<T, NW>(p);
+}
+// the same pass in its `rec` mode: the backward's recompute of a horizontal
+// direction's h (its own name in kernel traces and counter profiles)
+template <typename T, int NW>
+__global__ void __launch_bounds__(64 * NW) large_hrec_kernel(LargeHParams p) {
+  large_h_body<T, NW>(p);
+}
+
 // ---------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------
@@ -558,23 +580,25 @@ inline LargeGeom<T> large_geom(int H, int W) {
 }
 
 template <typename T, int WPD, bool BOTH, bool FIN>
-hipError_t launch_large_v_mode(const LargeVParams& p, hipStream_t st) {
-  hipLaunchKernelGGL((large_v_kernel<T, WPD, BOTH, FIN>), dim3((unsigned)(p.planes * (p.split ? 2 : 1))),
-                     dim3((BOTH ? 128 : 64) * WPD), 0, st, p);
+hipError_t launch_large_v_mode(const LargeVParams& p, bool rec, hipStream_t st) {
+  auto kern = rec ? large_vrec_kernel<T, WPD, BOTH, FIN> : large_v_kernel<T, WPD, BOTH, FIN>;
+  hipLaunchKernelGGL(kern, dim3((unsigned)(p.planes * (p.split ? 2 : 1))), dim3((BOTH ? 128 : 64) * WPD), 0, st,
+                     p);
   return hipGetLastError();
 }
 
+// rec: the backward's recompute (same kernel under its own name)
 template <typename T, int WPD>
-hipError_t launch_large_v(const LargeVParams& p, bool both, hipStream_t st) {
-  if (both) return p.final_out ? launch_large_v_mode<T, WPD, true, true>(p, st)
-                               : launch_large_v_mode<T, WPD, true, false>(p, st);
-  return p.final_out ? launch_large_v_mode<T, WPD, false, true>(p, st)
-                     : launch_large_v_mode<T, WPD, false, false>(p, st);
+hipError_t launch_large_v(const LargeVParams& p, bool both, hipStream_t st, bool rec = false) {
+  if (both) return p.final_out ? launch_large_v_mode<T, WPD, true, true>(p, rec, st)
+                               : launch_large_v_mode<T, WPD, true, false>(p, rec, st);
+  return p.final_out ? launch_large_v_mode<T, WPD, false, true>(p, rec, st)
+                     : launch_large_v_mode<T, WPD, false, false>(p, rec, st);
 }
 
 template <typename T, int NW>
 hipError_t launch_large_h_nw(const LargeHParams& p, int64_t grid, size_t lds, hipStream_t st) {
-  auto kern = large_h_kernel<T, NW>;
+  auto kern = p.rec ? large_hrec_kernel<T, NW> : large_h_kernel<T, NW>;
   if (lds > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;

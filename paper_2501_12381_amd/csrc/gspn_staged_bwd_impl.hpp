@@ -11,9 +11,10 @@
 //   du        du = dy * (h_T2B + h_B2T + h_L2R + h_R2L), fixed order;
 //   phase A   wave d runs the adjoint scan g = u dy + (transposed stencil of
 //             the next line's w and g), writes dw_k = g * h_prev(p+k-1) over
-//             the w_k entry it has just consumed, and g over h in its array;
-//   dx, dlam  from the fixed-order sum of g;
-//   epilogue  all threads: the dw maps LDS -> HBM.
+//             the w_k entry it has just consumed, and g over h in its array,
+//             then stores its three dw maps LDS -> HBM without waiting for the
+//             other waves;
+//   dx, dlam  from the fixed-order sum of g.
 // One workgroup per group of planes; with at most ~80 KB of LDS each, two
 // workgroups share a compute unit, so one's copies overlap the other's scans.
 #pragma once
@@ -384,23 +385,30 @@ __global__ void __launch_bounds__(256) staged_bwd_kernel(ResBwdParams p) {
       case 2: staged_adjoint<T, S, true, false, GRP>(s_udy + sg * HW, w3, harr, sl, lane_ok, p.gstart[2]); break;
       default: staged_adjoint<T, S, true, true, GRP>(s_udy + sg * HW, w3, harr, sl, lane_ok, p.gstart[3]); break;
     }
+    // this direction's three dw maps (written over its w maps by this wave
+    // alone) leave at once, while the other waves may still be scanning; the
+    // runs are contiguous in LDS and in global memory
+    uint4 r[3][NCH];
+#pragma unroll
+    for (int k = 0; k < 3; ++k)
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) {
+        const int v = c * 64 + lane < nv ? c * 64 + lane : nv - 1;
+        r[k][c] = reinterpret_cast<const uint4*>(lds4)[(SM_W + 3 * slot + k) * MV + v];
+      }
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+      T* dst = (T*)p.dw + (int64_t)(3 * slot + k) * p.npc + g0 * HW;  // dw maps: slot-major, packed like w
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) {
+        const int v = c * 64 + lane;
+        if (v < nv) *reinterpret_cast<uint4*>(dst + v * VE) = r[k][c];
+      }
+    }
   }
   lds_barrier();
 
-  // outputs: the dw maps (now in LDS) are read into registers first (clamped
-  // into the maps), then dx = lam * gsum and dlam = x * gsum, then every store;
-  // the dw runs are map-major and contiguous in LDS and in global memory
-  constexpr int ndw = 3 * ND, NMW = (ndw + 3) / 4;
-  uint4 r[NMW][NCH];
-#pragma unroll
-  for (int k = 0; k < NMW; ++k) {
-    const int wm = wave + 4 * k < ndw ? wave + 4 * k : ndw - 1;
-#pragma unroll
-    for (int c = 0; c < NCH; ++c) {
-      const int v = c * 64 + lane < nv ? c * 64 + lane : nv - 1;
-      r[k][c] = reinterpret_cast<const uint4*>(lds4)[(SM_W + wm) * MV + v];
-    }
-  }
+  // dx = lam * gsum and dlam = x * gsum (fixed-order sum of the directions' g)
   if (vreal) {
     Pack<T, VE> pl_, px;
     pl_.load(s_flat + SM_LAM * C::MS + iv * VE);
@@ -418,16 +426,6 @@ __global__ void __launch_bounds__(256) staged_bwd_kernel(ResBwdParams p) {
     const int64_t o = (g0 + vpl) * HW + ve0;
     stv<VE>((T*)p.dx + o, ra);
     stv<VE>((T*)p.dlam + o, rb);
-  }
-#pragma unroll
-  for (int k = 0; k < NMW; ++k) {
-    const int wm = wave + 4 * k;
-    T* dst = (T*)p.dw + (int64_t)wm * p.npc + g0 * HW;  // dw maps: slot-major, packed like w
-#pragma unroll
-    for (int c = 0; c < NCH; ++c) {
-      const int v = c * 64 + lane;
-      if (wm < ndw && v < nv) *reinterpret_cast<uint4*>(dst + v * VE) = r[k][c];
-    }
   }
 }
 

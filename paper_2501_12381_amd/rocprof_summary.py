@@ -110,7 +110,8 @@ def cmd_stats(args) -> int:
 
 
 def _match(name: str, pattern: str) -> bool:
-    return pattern in name
+    """pattern: substrings separated by '|'; the name matches if it contains any."""
+    return any(p in name for p in pattern.split("|"))
 
 
 def cmd_traffic(args) -> int:
