@@ -150,15 +150,20 @@ int check_ws(void* ws, size_t ws_bytes, size_t need,
   return GSPN_OK;
 }
 
+// Eq. 6 logits and edge renormalisation are taken by every family (except the
+// persistent 128 x 128 backward); the per-direction maps by the streaming
+// family only.  Every family takes groups.
+constexpr uint32_t kEq6Flags = GSPN_FLAG_W_LOGITS | GSPN_FLAG_EDGE_RENORM;
+
 bool resident_fits(const Problem& p, int dtype, bool backward) {
-  // the flags are implemented by the streaming family only; every family takes groups
-  if (p.flags) return false;
+  if (p.flags & ~kEq6Flags) return false;
+  if (p.flags && backward && p.H == 128 && p.W == 128) return false;
   if (p.grouped() && !(backward ? kResidentGroupsBwd : kResidentGroupsFwd)) return false;
   return gspn::resident_fits((int)p.H, (int)p.W, dtype, backward);
 }
 
 bool two_pass_fits(const Problem& p, int dtype, bool backward) {
-  if (p.flags || (p.grouped() && !kTwoPassGroups)) return false;
+  if ((p.flags & ~kEq6Flags) || (p.grouped() && !kTwoPassGroups)) return false;
   // the backward runs its horizontal directions on the two-pass kernels
   // (their vertical ones on the streaming kernels)
   if (backward && !(p.mask & (DIR_L2R | DIR_R2L))) return false;
@@ -274,6 +279,7 @@ int gspn_scan_fwd(const void* x, const void* w, const void* lam, const void* u, 
     r.x = x; r.lam = lam; r.w = w; r.u = u; r.y = y;
     r.mask = mask; r.planes = p.planes; r.H = (int)H; r.W = (int)W; r.dtype = dtype;
     r.group_h = p.gh; r.group_w = p.gw;
+    r.logits = p.logits(); r.renorm = (flags & GSPN_FLAG_EDGE_RENORM) ? 1 : 0;
     r.use_fixed = a == GSPN_ALGO_RESIDENT;
     r.stream = stream;
     return hip_status(resident_fwd(r));
@@ -286,6 +292,7 @@ int gspn_scan_fwd(const void* x, const void* w, const void* lam, const void* u, 
     l.state = (float*)((char*)workspace + two_pass_acc_bytes(p, mask));
     l.mask = mask; l.planes = p.planes; l.H = (int)H; l.W = (int)W; l.dtype = dtype;
     l.group_h = p.gh; l.group_w = p.gw;
+    l.logits = p.logits(); l.renorm = (flags & GSPN_FLAG_EDGE_RENORM) ? 1 : 0;
     l.stream = stream;
     return hip_status(large_fwd(l));
   }
@@ -370,6 +377,7 @@ int gspn_scan_bwd(const void* dy, const void* x, const void* w, const void* lam,
     r.dx = dx; r.dw = dw; r.dlam = dlam; r.du = du;
     r.mask = mask; r.planes = p.planes; r.H = (int)H; r.W = (int)W; r.dtype = dtype;
     r.group_h = p.gh; r.group_w = p.gw;
+    r.logits = p.logits(); r.renorm = (flags & GSPN_FLAG_EDGE_RENORM) ? 1 : 0;
     r.use_staged = a == GSPN_ALGO_RESIDENT;
     r.stream = stream;
     return hip_status(resident_bwd(r));
@@ -399,6 +407,7 @@ int gspn_scan_bwd(const void* dy, const void* x, const void* w, const void* lam,
       l.dir = d == 3 ? 1 : 0;
       l.planes = p.planes; l.H = (int)H; l.W = (int)W;
       l.group = p.gw;
+      l.logits = p.logits(); l.renorm = (flags & GSPN_FLAG_EDGE_RENORM) ? 1 : 0;
       l.stream = stream;
       st = hip_status(large_bwd_h(l, dtype));
       if (st != GSPN_OK) return st;
@@ -414,6 +423,7 @@ int gspn_scan_bwd(const void* dy, const void* x, const void* w, const void* lam,
       v.h_t2b = hv[0]; v.h_b2t = hv[1];
       v.planes = p.planes; v.H = (int)H; v.W = (int)W;
       v.group = p.gh;
+      v.logits = p.logits(); v.renorm = (flags & GSPN_FLAG_EDGE_RENORM) ? 1 : 0;
       v.stream = stream;
       st = hip_status(large_bwd_v_rec(v, dtype));
       if (st != GSPN_OK) return st;
@@ -426,6 +436,7 @@ int gspn_scan_bwd(const void* dy, const void* x, const void* w, const void* lam,
       r.gsum = gsum;
       r.planes = p.planes; r.H = (int)H; r.W = (int)W;
       r.group = p.gh;
+      r.logits = p.logits(); r.renorm = (flags & GSPN_FLAG_EDGE_RENORM) ? 1 : 0;
       r.stream = stream;
       st = hip_status(large_bwd_v_adj(r, dtype));
       if (st != GSPN_OK) return st;

@@ -124,6 +124,43 @@ __device__ __forceinline__ bool group_start(int line, int G, bool rev) {
   return rev ? ((line + 1) % G == 0) : (line % G == 0);
 }
 
+// Eq. 6: the three logits of one pixel -> its three weights (sigmoid, then
+// normalised over the neighbours that count: all three, or with edge
+// renormalisation the ones on the line).  Also returns the sigmoids and the
+// normaliser for the Jacobian of the backward.  The reciprocals are the
+// hardware's (v_rcp_f32, within 1 ulp): an IEEE division would cost a dozen
+// instructions per weight in the kernels' line steps.  A normaliser that
+// underflows to zero (every sigmoid zero) is clamped, giving zero weights.
+struct Norm3 {
+  float w[3], sg[3], m[3], inv;
+};
+__device__ __forceinline__ Norm3 normalize3(float l0, float l1, float l2, bool first_pos, bool last_pos,
+                                            bool renorm) {
+  Norm3 r;
+  r.sg[0] = __builtin_amdgcn_rcpf(1.f + __expf(-l0));
+  r.sg[1] = __builtin_amdgcn_rcpf(1.f + __expf(-l1));
+  r.sg[2] = __builtin_amdgcn_rcpf(1.f + __expf(-l2));
+  r.m[0] = (renorm && first_pos) ? 0.f : 1.f;
+  r.m[1] = 1.f;
+  r.m[2] = (renorm && last_pos) ? 0.f : 1.f;
+  const float s0 = r.m[0] * r.sg[0], s1 = r.sg[1], s2 = r.m[2] * r.sg[2];
+  r.inv = __builtin_amdgcn_rcpf(fmaxf(s0 + s1 + s2, 1e-30f));
+  r.w[0] = s0 * r.inv;
+  r.w[1] = s1 * r.inv;
+  r.w[2] = s2 * r.inv;
+  return r;
+}
+
+// The Jacobian of the normalisation applied to the gradients e_k of the three
+// weights: dl_k = m_k sig_k (1 - sig_k) (e_k - sum_j w_j e_j) / S, where S is
+// the normaliser (r.inv = 1 / S).
+__device__ __forceinline__ void norm3_vjp(const Norm3& r, float& e0, float& e1, float& e2) {
+  const float inner = r.w[0] * e0 + r.w[1] * e1 + r.w[2] * e2;
+  e0 = r.m[0] * r.sg[0] * (1.f - r.sg[0]) * (e0 - inner) * r.inv;
+  e1 = r.m[1] * r.sg[1] * (1.f - r.sg[1]) * (e1 - inner) * r.inv;
+  e2 = r.m[2] * r.sg[2] * (1.f - r.sg[2]) * (e2 - inner) * r.inv;
+}
+
 // Calls f(std::integral_constant<int, i>) for i = B .. E-1 (compile-time indices,
 // fully unrolled by construction, where a large unrolled loop body may not be).
 template <int B, int E, typename F>

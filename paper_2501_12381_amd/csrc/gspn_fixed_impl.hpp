@@ -62,10 +62,11 @@ struct FixedCfg {
 // accumulator come from LDS, read G lines ahead of their use (never across the
 // middle barrier), so each input is read from HBM once.
 // GRP: local GSPN; bit l of gst is set when line l starts a group (the state
-// restarts from zero there).
-template <typename T, int S, bool HZ, bool REV, bool PRESENT, bool GRP>
+// restarts from zero there).  LG: the weight maps hold Eq. 6 logits,
+// normalised as they are unpacked (renorm: over the on-line neighbours).
+template <typename T, int S, bool HZ, bool REV, bool PRESENT, bool GRP, bool LG>
 __device__ __forceinline__ void fixed_phase(const T* const (&pbase)[5], float* __restrict__ acc,
-                                            float* __restrict__ lxa, int sl, uint64_t gst) {
+                                            float* __restrict__ lxa, int sl, uint64_t gst, bool renorm) {
   using C = FixedCfg<T, S>;
   constexpr int TL = HZ ? C::THZ : 1;   // lines per tile
   constexpr int R = HZ ? C::RH : C::RV; // tiles in flight
@@ -147,6 +148,12 @@ __device__ __forceinline__ void fixed_phase(const T* const (&pbase)[5], float* _
         a = HZ ? ring[slot][2].get(e) : v1[2];
         b = HZ ? ring[slot][3].get(e) : v1[3];
         c = HZ ? ring[slot][4].get(e) : v1[4];
+        if constexpr (LG) {
+          const Norm3 r = normalize3(a, b, c, sl == 0, sl == S - 1, renorm);
+          a = r.w[0];
+          b = r.w[1];
+          c = r.w[2];
+        }
         if (GRP && ((gst >> line_of(s)) & 1)) hp = 0.f;
         const float hl = from_prev_lane(hp), hr = from_next_lane(hp);
         float v = fmaf(a, hl, lx);
@@ -166,7 +173,7 @@ __device__ __forceinline__ void fixed_phase(const T* const (&pbase)[5], float* _
   }
 }
 
-template <typename T, int S, bool GRP>
+template <typename T, int S, bool GRP, bool LG>
 __global__ void __launch_bounds__(128, (FixedCfg<T, S>::SEG < 64 ? 4 : 2))
 fixed_fwd_kernel(ResFwdParams p) {
   using C = FixedCfg<T, S>;
@@ -179,6 +186,7 @@ fixed_fwd_kernel(ResFwdParams p) {
   const int64_t plane = (g0 + seg < p.planes) ? g0 + seg : p.planes - 1;
   float* acc = lds + seg * C::ACC;
   float* lxa = lds + (PPW + seg) * C::ACC;
+  const bool rn = LG && p.renorm;
 
   // phase V: wave 0 top-to-bottom, wave 1 bottom-to-top
   {
@@ -187,11 +195,11 @@ fixed_fwd_kernel(ResFwdParams p) {
     const T* pb[5] = {(const T*)p.x + plane * HW, (const T*)p.lam + plane * HW, w0, w0 + p.npc, w0 + 2 * p.npc};
     const uint64_t gst = p.gstart[wave][0];
     if (wave == 0) {
-      if (slot >= 0) fixed_phase<T, S, false, false, true, GRP>(pb, acc, lxa, sl, gst);
-      else fixed_phase<T, S, false, false, false, GRP>(pb, acc, lxa, sl, gst);
+      if (slot >= 0) fixed_phase<T, S, false, false, true, GRP, LG>(pb, acc, lxa, sl, gst, rn);
+      else fixed_phase<T, S, false, false, false, GRP, LG>(pb, acc, lxa, sl, gst, rn);
     } else {
-      if (slot >= 0) fixed_phase<T, S, false, true, true, GRP>(pb, acc, lxa, sl, gst);
-      else fixed_phase<T, S, false, true, false, GRP>(pb, acc, lxa, sl, gst);
+      if (slot >= 0) fixed_phase<T, S, false, true, true, GRP, LG>(pb, acc, lxa, sl, gst, rn);
+      else fixed_phase<T, S, false, true, false, GRP, LG>(pb, acc, lxa, sl, gst, rn);
     }
   }
   __syncthreads();
@@ -226,8 +234,8 @@ fixed_fwd_kernel(ResFwdParams p) {
       const T* pb[5] = {(const T*)p.x + plane * HW, (const T*)p.lam + plane * HW, w0, w0 + p.npc,
                         w0 + 2 * p.npc};
       const uint64_t gst = p.gstart[2 + wave][0];
-      if (wave == 0) fixed_phase<T, S, true, false, true, GRP>(pb, acc, lxa, sl, gst);
-      else fixed_phase<T, S, true, true, true, GRP>(pb, acc, lxa, sl, gst);
+      if (wave == 0) fixed_phase<T, S, true, false, true, GRP, LG>(pb, acc, lxa, sl, gst, rn);
+      else fixed_phase<T, S, true, true, true, GRP, LG>(pb, acc, lxa, sl, gst, rn);
     }
   }
   __syncthreads();
@@ -280,7 +288,8 @@ inline bool fixed_size_supported(int H, int W) {
 template <typename T, int S>
 hipError_t launch_fixed(const ResFwdParams& p, hipStream_t st) {
   using C = FixedCfg<T, S>;
-  auto kern = p.grouped ? fixed_fwd_kernel<T, S, true> : fixed_fwd_kernel<T, S, false>;
+  auto kern = p.logits ? (p.grouped ? fixed_fwd_kernel<T, S, true, true> : fixed_fwd_kernel<T, S, false, true>)
+                       : (p.grouped ? fixed_fwd_kernel<T, S, true, false> : fixed_fwd_kernel<T, S, false, false>);
   if (C::LDS_BYTES > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
                                        C::LDS_BYTES);

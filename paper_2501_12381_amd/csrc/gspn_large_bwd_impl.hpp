@@ -53,11 +53,13 @@ struct LargeHAdjParams {
   // bit i: window column i takes nothing from the next line (that line starts
   // a group); bit i of gmask: window column i starts a group (zero previous state)
   uint64_t zmask, gmask;
+  int renorm;          // Eq. 6 logits (LG kernels): normalise over on-line neighbours only
 };
 
 // DIR 0: left-to-right (its adjoint walks the blocks and columns right to left);
-// DIR 1: right-to-left (adjoint left to right).
-template <typename T, int NW, int DIR>
+// DIR 1: right-to-left (adjoint left to right).  LG: the weight maps hold
+// Eq. 6 logits; dw becomes their gradient.
+template <typename T, int NW, int DIR, bool LG>
 __global__ void __launch_bounds__(64 * NW) large_hadj_kernel(LargeHAdjParams p) {
   using C = LargeCfg<T>;
   constexpr int K = C::KH, HV = C::HV, VE = C::VE;
@@ -181,15 +183,24 @@ __global__ void __launch_bounds__(64 * NW) large_hadj_kernel(LargeHAdjParams p) 
     const float dyv = tile[0][ti / VE].get(ti % VE), uv = tile[1][ti / VE].get(ti % VE);
     float g = fmaf(uv, dyv, gin);
     g = row_ok ? g : 0.f;
-    a0 = tile[2][ti / VE].get(ti % VE) * g;
-    a1 = tile[3][ti / VE].get(ti % VE) * g;
-    a2 = tile[4][ti / VE].get(ti % VE) * g;
+    float wa = tile[2][ti / VE].get(ti % VE), wb = tile[3][ti / VE].get(ti % VE), wc = tile[4][ti / VE].get(ti % VE);
+    Norm3 nr;
+    if constexpr (LG) {
+      nr = normalize3(wa, wb, wc, r == 0, r == H - 1, p.renorm != 0);
+      wa = nr.w[0];
+      wb = nr.w[1];
+      wc = nr.w[2];
+    }
+    a0 = wa * g;
+    a1 = wb * g;
+    a2 = wc * g;
     edge[par ? eo1 : eo0] = lane == 0 ? a0 : a2;
     // dw from the previous column's h on rows p-1, p, p+1 (zero at a group start)
     const bool gr = (gm >> ti) & 1;
     const int hc = ti + HOFF + PREV;
     const float hl = gr ? 0.f : hrow[hc - HP], hm = gr ? 0.f : hrow[hc], hr = gr ? 0.f : hrow[hc + HP];
-    const float d0 = g * hl, d1 = g * hm, d2 = g * hr;
+    float d0 = g * hl, d1 = g * hm, d2 = g * hr;
+    if constexpr (LG) norm3_vjp(nr, d0, d1, d2);
     if constexpr (sizeof(T) == 2) {
       // a word holds columns 2j (low half) and 2j + 1; the second one done completes it
       constexpr bool second = DIR ? (ti & 1) : !(ti & 1);
@@ -266,8 +277,10 @@ __global__ void __launch_bounds__(64 * NW) large_hadj_kernel(LargeHAdjParams p) 
 // ---------------------------------------------------------------------------
 
 template <typename T, int NW>
-hipError_t launch_large_hadj_nw(const LargeHAdjParams& p, int dir, int64_t grid, size_t lds, hipStream_t st) {
-  auto kern = dir ? large_hadj_kernel<T, NW, 1> : large_hadj_kernel<T, NW, 0>;
+hipError_t launch_large_hadj_nw(const LargeHAdjParams& p, int dir, int64_t grid, size_t lds, bool lg,
+                                hipStream_t st) {
+  auto kern = lg ? (dir ? large_hadj_kernel<T, NW, 1, true> : large_hadj_kernel<T, NW, 0, true>)
+                 : (dir ? large_hadj_kernel<T, NW, 1, false> : large_hadj_kernel<T, NW, 0, false>);
   if (lds > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
@@ -277,16 +290,17 @@ hipError_t launch_large_hadj_nw(const LargeHAdjParams& p, int dir, int64_t grid,
 }
 
 template <typename T>
-hipError_t launch_large_hadj(const LargeHAdjParams& p, int dir, int nw, int64_t grid, size_t lds, hipStream_t st) {
+hipError_t launch_large_hadj(const LargeHAdjParams& p, int dir, int nw, int64_t grid, size_t lds, bool lg,
+                             hipStream_t st) {
   switch (nw) {
-    case 1: return launch_large_hadj_nw<T, 1>(p, dir, grid, lds, st);
-    case 2: return launch_large_hadj_nw<T, 2>(p, dir, grid, lds, st);
-    case 3: return launch_large_hadj_nw<T, 3>(p, dir, grid, lds, st);
-    case 4: return launch_large_hadj_nw<T, 4>(p, dir, grid, lds, st);
-    case 5: return launch_large_hadj_nw<T, 5>(p, dir, grid, lds, st);
-    case 6: return launch_large_hadj_nw<T, 6>(p, dir, grid, lds, st);
-    case 7: return launch_large_hadj_nw<T, 7>(p, dir, grid, lds, st);
-    case 8: return launch_large_hadj_nw<T, 8>(p, dir, grid, lds, st);
+    case 1: return launch_large_hadj_nw<T, 1>(p, dir, grid, lds, lg, st);
+    case 2: return launch_large_hadj_nw<T, 2>(p, dir, grid, lds, lg, st);
+    case 3: return launch_large_hadj_nw<T, 3>(p, dir, grid, lds, lg, st);
+    case 4: return launch_large_hadj_nw<T, 4>(p, dir, grid, lds, lg, st);
+    case 5: return launch_large_hadj_nw<T, 5>(p, dir, grid, lds, lg, st);
+    case 6: return launch_large_hadj_nw<T, 6>(p, dir, grid, lds, lg, st);
+    case 7: return launch_large_hadj_nw<T, 7>(p, dir, grid, lds, lg, st);
+    case 8: return launch_large_hadj_nw<T, 8>(p, dir, grid, lds, lg, st);
     default: return hipErrorInvalidValue;
   }
 }
@@ -322,6 +336,7 @@ hipError_t large_bwd_h_t(const LargeBwdHArgs& a) {
   h.acc_b = nullptr;
   h.rec = 1;
   h.hbuf = a.hbuf;
+  h.renorm = a.renorm;
   for (int j = 0; j < g.nblk; ++j) {
     const int blk = a.dir ? g.nblk - 1 - j : j;
     const int ws = window(blk);
@@ -332,7 +347,7 @@ hipError_t large_bwd_h_t(const LargeBwdHArgs& a) {
     h.step = j;
     h.gmask[0] = a.dir ? 0 : m;
     h.gmask[1] = a.dir ? m : 0;
-    hipError_t e = launch_large_h<T>(h, g.nw, grid, g.lds_h, st);
+    hipError_t e = launch_large_h<T>(h, g.nw, grid, g.lds_h, a.logits != 0, st);
     if (e != hipSuccess) return e;
   }
 
@@ -341,6 +356,7 @@ hipError_t large_bwd_h_t(const LargeBwdHArgs& a) {
   p.dy = a.dy; p.u = a.u; p.w = a.w; p.dw = a.dw; p.hbuf = a.hbuf; p.gsum = a.gsum; p.state = a.state;
   p.planes = a.planes; p.npc = npc; p.H = a.H; p.W = a.W;
   p.first = a.first;
+  p.renorm = a.renorm;
   p.nblk = g.nblk;
   p.band_rows = g.band_rows; p.nbands = g.nbands; p.halo = g.halo;
   const size_t lds = ((size_t)(g.band_rows + 2) * (K + 5) + 4 * 8 + 64) * sizeof(float);
@@ -357,7 +373,7 @@ hipError_t large_bwd_h_t(const LargeBwdHArgs& a) {
     p.step = j;
     p.zmask = zm;
     p.gmask = gm;
-    hipError_t e = launch_large_hadj<T>(p, a.dir, g.nw, grid, lds, st);
+    hipError_t e = launch_large_hadj<T>(p, a.dir, g.nw, grid, lds, a.logits != 0, st);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
@@ -377,12 +393,13 @@ hipError_t large_bwd_v_rec_t(const LargeBwdVArgs& a) {
   v.final_out = 0;
   v.split = both ? 1 : 0;
   v.grp = (a.group > 0 && a.group < a.H) ? a.group : a.H;
+  v.renorm = a.renorm;
   if (both && 2 * a.planes > 0x7fffffffLL) return hipErrorInvalidConfiguration;
   hipStream_t st = (hipStream_t)a.stream;
   switch (g.wpd) {
-    case 1: return launch_large_v<T, 1>(v, false, st, true);
-    case 2: return launch_large_v<T, 2>(v, false, st, true);
-    case 4: return launch_large_v<T, 4>(v, false, st, true);
+    case 1: return launch_large_v<T, 1>(v, false, st, true, a.logits != 0);
+    case 2: return launch_large_v<T, 2>(v, false, st, true, a.logits != 0);
+    case 4: return launch_large_v<T, 4>(v, false, st, true, a.logits != 0);
     default: return hipErrorInvalidValue;
   }
 }
@@ -410,9 +427,11 @@ struct LargeVAdjParams {
   int H, W;
   int slot[2];          // weight slots of top-to-bottom, bottom-to-top (-1 absent)
   int grp;              // rows per local-GSPN group (H: global)
+  int renorm;           // Eq. 6 logits (LG kernels): normalise over on-line neighbours only
 };
 
-template <typename T, int WPD, bool BOTH>
+// LG: the weight maps hold Eq. 6 logits; dw becomes their gradient.
+template <typename T, int WPD, bool BOTH, bool LG>
 __global__ void __launch_bounds__((BOTH ? 128 : 64) * WPD, 2) large_vadj_kernel(LargeVAdjParams p) {
   using C = LargeCfg<T>;
   // rings: R rows of the bf16/fp32 input maps, RH rows of h, RA rows of gsum
@@ -596,15 +615,24 @@ __global__ void __launch_bounds__((BOTH ? 128 : 64) * WPD, 2) large_vadj_kernel(
       float dv[3][G], go[G];
 #pragma unroll
       for (int j = 0; j < G; ++j) {
-        a0[q][j] = v[2][q].get(j) * g[j];
-        a1[q][j] = v[3][q].get(j) * g[j];
-        a2[q][j] = v[4][q].get(j) * g[j];
+        float wa = v[2][q].get(j), wb = v[3][q].get(j), wc = v[4][q].get(j);
+        Norm3 nr;
+        if constexpr (LG) {
+          nr = normalize3(wa, wb, wc, po[q] + j == 0, po[q] + j == W - 1, p.renorm != 0);
+          wa = nr.w[0];
+          wb = nr.w[1];
+          wc = nr.w[2];
+        }
+        a0[q][j] = wa * g[j];
+        a1[q][j] = wb * g[j];
+        a2[q][j] = wc * g[j];
         const float hm = hzero ? 0.f : hv[q][j];
         const float hlv = hzero ? 0.f : (j == 0 ? hl[q] : hv[q][j - 1]);
         const float hrv = hzero ? 0.f : (j == G - 1 ? hr[q] : hv[q][j + 1]);
         dv[0][j] = g[j] * hlv;
         dv[1][j] = g[j] * hm;
         dv[2][j] = g[j] * hrv;
+        if constexpr (LG) norm3_vjp(nr, dv[0][j], dv[1][j], dv[2][j]);
         go[j] = gring[k % RA][q][j] + g[j];
       }
       if (ok) {
@@ -658,9 +686,9 @@ __global__ void __launch_bounds__((BOTH ? 128 : 64) * WPD, 2) large_vadj_kernel(
 }
 
 template <typename T, int WPD, bool BOTH>
-hipError_t launch_large_vadj_mode(const LargeVAdjParams& p, hipStream_t st) {
-  hipLaunchKernelGGL((large_vadj_kernel<T, WPD, BOTH>), dim3((unsigned)p.planes), dim3((BOTH ? 128 : 64) * WPD),
-                     0, st, p);
+hipError_t launch_large_vadj_mode(const LargeVAdjParams& p, bool lg, hipStream_t st) {
+  auto kern = lg ? large_vadj_kernel<T, WPD, BOTH, true> : large_vadj_kernel<T, WPD, BOTH, false>;
+  hipLaunchKernelGGL(kern, dim3((unsigned)p.planes), dim3((BOTH ? 128 : 64) * WPD), 0, st, p);
   return hipGetLastError();
 }
 
@@ -676,12 +704,13 @@ hipError_t large_bwd_v_adj_t(const LargeBwdVAdjArgs& a) {
   p.planes = a.planes; p.npc = a.planes * (int64_t)a.H * a.W; p.H = a.H; p.W = a.W;
   p.slot[0] = a.slot_t2b; p.slot[1] = a.slot_b2t;
   p.grp = (a.group > 0 && a.group < a.H) ? a.group : a.H;
-  const bool both = a.slot_t2b >= 0 && a.slot_b2t >= 0;
+  p.renorm = a.renorm;
+  const bool both = a.slot_t2b >= 0 && a.slot_b2t >= 0, lg = a.logits != 0;
   hipStream_t st = (hipStream_t)a.stream;
   switch (g.wpd) {
-    case 1: return both ? launch_large_vadj_mode<T, 1, true>(p, st) : launch_large_vadj_mode<T, 1, false>(p, st);
-    case 2: return both ? launch_large_vadj_mode<T, 2, true>(p, st) : launch_large_vadj_mode<T, 2, false>(p, st);
-    case 4: return both ? launch_large_vadj_mode<T, 4, true>(p, st) : launch_large_vadj_mode<T, 4, false>(p, st);
+    case 1: return both ? launch_large_vadj_mode<T, 1, true>(p, lg, st) : launch_large_vadj_mode<T, 1, false>(p, lg, st);
+    case 2: return both ? launch_large_vadj_mode<T, 2, true>(p, lg, st) : launch_large_vadj_mode<T, 2, false>(p, lg, st);
+    case 4: return both ? launch_large_vadj_mode<T, 4, true>(p, lg, st) : launch_large_vadj_mode<T, 4, false>(p, lg, st);
     default: return hipErrorInvalidValue;
   }
 }

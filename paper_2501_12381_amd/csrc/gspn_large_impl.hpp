@@ -64,6 +64,7 @@ struct LargeVParams {
                      // (blockIdx / planes), bottom-to-top writing its h here
   int split;
   int grp;           // rows per local-GSPN group (H: the global scan)
+  int renorm;        // Eq. 6 logits (LG kernels): normalise over on-line neighbours only
 };
 
 // Layout of a row over a wave: the wave's span of 64 * NP positions is cut into
@@ -74,7 +75,8 @@ struct LargeVParams {
 // previous chunk (a lane read), of the previous wave (LDS) or padding.
 //
 // BOTH: both vertical directions are present; FIN: write y (no pass H follows).
-template <typename T, int WPD, bool BOTH, bool FIN>
+// LG: the weight maps hold Eq. 6 logits, normalised as they are unpacked.
+template <typename T, int WPD, bool BOTH, bool FIN, bool LG>
 __device__ __forceinline__ void large_v_body(const LargeVParams& p) {
   using C = LargeCfg<T>;
   constexpr int NP = C::NPV, R = C::RV, RA = C::RA;
@@ -209,10 +211,17 @@ __device__ __forceinline__ void large_v_body(const LargeVParams& p) {
       for (int j = 0; j < G; ++j) {
         const float hl = j == 0 ? el[q] : hp[q][j - 1];
         const float hr = j == G - 1 ? er[q] : hp[q][j + 1];
+        float wa = v[2][q].get(j), wb = v[3][q].get(j), wc = v[4][q].get(j);
+        if constexpr (LG) {
+          const Norm3 nr = normalize3(wa, wb, wc, po[q] + j == 0, po[q] + j == W - 1, p.renorm != 0);
+          wa = nr.w[0];
+          wb = nr.w[1];
+          wc = nr.w[2];
+        }
         float r = v[1][q].get(j) * v[0][q].get(j);
-        r = fmaf(v[2][q].get(j), hl, r);
-        r = fmaf(v[3][q].get(j), hp[q][j], r);
-        r = fmaf(v[4][q].get(j), hr, r);
+        r = fmaf(wa, hl, r);
+        r = fmaf(wb, hp[q][j], r);
+        r = fmaf(wc, hr, r);
         h[q][j] = ok ? r : 0.f;
       }
     }
@@ -304,15 +313,15 @@ __device__ __forceinline__ void large_v_body(const LargeVParams& p) {
     }
 }
 
-template <typename T, int WPD, bool BOTH, bool FIN>
+template <typename T, int WPD, bool BOTH, bool FIN, bool LG>
 __global__ void __launch_bounds__(128 * WPD, 2) large_v_kernel(LargeVParams p) {
-  large_v_body<T, WPD, BOTH, FIN>(p);
+  large_v_body<T, WPD, BOTH, FIN, LG>(p);
 }
 // the same pass as the backward's recompute of the vertical directions' h
 // (its own name in kernel traces and counter profiles)
-template <typename T, int WPD, bool BOTH, bool FIN>
+template <typename T, int WPD, bool BOTH, bool FIN, bool LG>
 __global__ void __launch_bounds__(128 * WPD, 2) large_vrec_kernel(LargeVParams p) {
-  large_v_body<T, WPD, BOTH, FIN>(p);
+  large_v_body<T, WPD, BOTH, FIN, LG>(p);
 }
 
 // ---------------------------------------------------------------------------
@@ -343,9 +352,11 @@ struct LargeHParams {
   // to hbuf; nothing is multiplied by u
   int rec;
   float* hbuf;
+  int renorm;         // Eq. 6 logits (LG kernels): normalise over on-line neighbours only
 };
 
-template <typename T, int NW>
+// LG: the weight maps hold Eq. 6 logits, normalised as they are unpacked.
+template <typename T, int NW, bool LG>
 __device__ __forceinline__ void large_h_body(const LargeHParams& p) {
   using C = LargeCfg<T>;
   constexpr int K = C::KH, HV = C::HV, VE = C::VE, KP = K + 1;
@@ -466,8 +477,14 @@ __device__ __forceinline__ void large_h_body(const LargeHParams& p) {
         if (lane == 63) dn = (wave < NW - 1 && !rst) ? nd : 0.f;
       }
       const float xv = tile[0][ti / VE].get(ti % VE), lv = tile[1][ti / VE].get(ti % VE);
-      const float a = tile[2][ti / VE].get(ti % VE), bw = tile[3][ti / VE].get(ti % VE),
-                  cw = tile[4][ti / VE].get(ti % VE);
+      float a = tile[2][ti / VE].get(ti % VE), bw = tile[3][ti / VE].get(ti % VE),
+            cw = tile[4][ti / VE].get(ti % VE);
+      if constexpr (LG) {
+        const Norm3 nr = normalize3(a, bw, cw, r == 0, r == H - 1, p.renorm != 0);
+        a = nr.w[0];
+        bw = nr.w[1];
+        cw = nr.w[2];
+      }
       float h = lv * xv;
       h = fmaf(a, up, h);
       h = fmaf(bw, hp, h);
@@ -527,15 +544,15 @@ __device__ __forceinline__ void large_h_body(const LargeHParams& p) {
   }
 }
 
-template <typename T, int NW>
+template <typename T, int NW, bool LG>
 __global__ void __launch_bounds__(64 * NW) large_h_kernel(LargeHParams p) {
-  large_h_body<T, NW>(p);
+  large_h_body<T, NW, LG>(p);
 }
 // the same pass in its `rec` mode: the backward's recompute of a horizontal
 // direction's h (its own name in kernel traces and counter profiles)
-template <typename T, int NW>
+template <typename T, int NW, bool LG>
 __global__ void __launch_bounds__(64 * NW) large_hrec_kernel(LargeHParams p) {
-  large_h_body<T, NW>(p);
+  large_h_body<T, NW, LG>(p);
 }
 
 // ---------------------------------------------------------------------------
@@ -580,25 +597,28 @@ inline LargeGeom<T> large_geom(int H, int W) {
 }
 
 template <typename T, int WPD, bool BOTH, bool FIN>
-hipError_t launch_large_v_mode(const LargeVParams& p, bool rec, hipStream_t st) {
-  auto kern = rec ? large_vrec_kernel<T, WPD, BOTH, FIN> : large_v_kernel<T, WPD, BOTH, FIN>;
+hipError_t launch_large_v_mode(const LargeVParams& p, bool rec, bool lg, hipStream_t st) {
+  auto kern = lg ? (rec ? large_vrec_kernel<T, WPD, BOTH, FIN, true> : large_v_kernel<T, WPD, BOTH, FIN, true>)
+                 : (rec ? large_vrec_kernel<T, WPD, BOTH, FIN, false> : large_v_kernel<T, WPD, BOTH, FIN, false>);
   hipLaunchKernelGGL(kern, dim3((unsigned)(p.planes * (p.split ? 2 : 1))), dim3((BOTH ? 128 : 64) * WPD), 0, st,
                      p);
   return hipGetLastError();
 }
 
-// rec: the backward's recompute (same kernel under its own name)
+// rec: the backward's recompute (same kernel under its own name); lg: the
+// weight maps hold Eq. 6 logits
 template <typename T, int WPD>
-hipError_t launch_large_v(const LargeVParams& p, bool both, hipStream_t st, bool rec = false) {
-  if (both) return p.final_out ? launch_large_v_mode<T, WPD, true, true>(p, rec, st)
-                               : launch_large_v_mode<T, WPD, true, false>(p, rec, st);
-  return p.final_out ? launch_large_v_mode<T, WPD, false, true>(p, rec, st)
-                     : launch_large_v_mode<T, WPD, false, false>(p, rec, st);
+hipError_t launch_large_v(const LargeVParams& p, bool both, hipStream_t st, bool rec, bool lg) {
+  if (both) return p.final_out ? launch_large_v_mode<T, WPD, true, true>(p, rec, lg, st)
+                               : launch_large_v_mode<T, WPD, true, false>(p, rec, lg, st);
+  return p.final_out ? launch_large_v_mode<T, WPD, false, true>(p, rec, lg, st)
+                     : launch_large_v_mode<T, WPD, false, false>(p, rec, lg, st);
 }
 
 template <typename T, int NW>
-hipError_t launch_large_h_nw(const LargeHParams& p, int64_t grid, size_t lds, hipStream_t st) {
-  auto kern = p.rec ? large_hrec_kernel<T, NW> : large_h_kernel<T, NW>;
+hipError_t launch_large_h_nw(const LargeHParams& p, int64_t grid, size_t lds, bool lg, hipStream_t st) {
+  auto kern = lg ? (p.rec ? large_hrec_kernel<T, NW, true> : large_h_kernel<T, NW, true>)
+                 : (p.rec ? large_hrec_kernel<T, NW, false> : large_h_kernel<T, NW, false>);
   if (lds > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
@@ -608,16 +628,16 @@ hipError_t launch_large_h_nw(const LargeHParams& p, int64_t grid, size_t lds, hi
 }
 
 template <typename T>
-hipError_t launch_large_h(const LargeHParams& p, int nw, int64_t grid, size_t lds, hipStream_t st) {
+hipError_t launch_large_h(const LargeHParams& p, int nw, int64_t grid, size_t lds, bool lg, hipStream_t st) {
   switch (nw) {
-    case 1: return launch_large_h_nw<T, 1>(p, grid, lds, st);
-    case 2: return launch_large_h_nw<T, 2>(p, grid, lds, st);
-    case 3: return launch_large_h_nw<T, 3>(p, grid, lds, st);
-    case 4: return launch_large_h_nw<T, 4>(p, grid, lds, st);
-    case 5: return launch_large_h_nw<T, 5>(p, grid, lds, st);
-    case 6: return launch_large_h_nw<T, 6>(p, grid, lds, st);
-    case 7: return launch_large_h_nw<T, 7>(p, grid, lds, st);
-    case 8: return launch_large_h_nw<T, 8>(p, grid, lds, st);
+    case 1: return launch_large_h_nw<T, 1>(p, grid, lds, lg, st);
+    case 2: return launch_large_h_nw<T, 2>(p, grid, lds, lg, st);
+    case 3: return launch_large_h_nw<T, 3>(p, grid, lds, lg, st);
+    case 4: return launch_large_h_nw<T, 4>(p, grid, lds, lg, st);
+    case 5: return launch_large_h_nw<T, 5>(p, grid, lds, lg, st);
+    case 6: return launch_large_h_nw<T, 6>(p, grid, lds, lg, st);
+    case 7: return launch_large_h_nw<T, 7>(p, grid, lds, lg, st);
+    case 8: return launch_large_h_nw<T, 8>(p, grid, lds, lg, st);
     default: return hipErrorInvalidValue;
   }
 }
@@ -644,14 +664,15 @@ hipError_t large_fwd_t(const LargeFwdArgs& a) {
     // so the grid has no partly filled last round of whole planes)
     v.grp = (a.group_h > 0 && a.group_h < a.H) ? a.group_h : a.H;
     v.split = slot[0] >= 0 && slot[1] >= 0 && has_h && a.acc_b != nullptr;
+    v.renorm = a.renorm;
     v.acc_b = a.acc_b;
     if (v.split && 2 * a.planes > 0x7fffffffLL) return hipErrorInvalidConfiguration;
     const bool both = slot[0] >= 0 && slot[1] >= 0 && !v.split;
     hipError_t e;
     switch (g.wpd) {
-      case 1: e = launch_large_v<T, 1>(v, both, st); break;
-      case 2: e = launch_large_v<T, 2>(v, both, st); break;
-      case 4: e = launch_large_v<T, 4>(v, both, st); break;
+      case 1: e = launch_large_v<T, 1>(v, both, st, false, a.logits != 0); break;
+      case 2: e = launch_large_v<T, 2>(v, both, st, false, a.logits != 0); break;
+      case 4: e = launch_large_v<T, 4>(v, both, st, false, a.logits != 0); break;
       default: e = hipErrorInvalidValue;
     }
     if (e != hipSuccess) return e;
@@ -667,6 +688,7 @@ hipError_t large_fwd_t(const LargeFwdArgs& a) {
   h.half = both ? g.nblk / 2 + h.delay : 0;
   h.band_rows = g.band_rows; h.nbands = g.nbands; h.halo = g.halo;
   h.has_v = has_v ? 1 : 0;
+  h.renorm = a.renorm;
   h.acc_b = (slot[0] >= 0 && slot[1] >= 0 && a.acc_b != nullptr) ? a.acc_b : nullptr;
   const int64_t grid = (int64_t)g.nbands * a.planes * (both ? 2 : 1);
   if (grid > 0x7fffffffLL) return hipErrorInvalidConfiguration;
@@ -689,7 +711,7 @@ hipError_t large_fwd_t(const LargeFwdArgs& a) {
     h.step = j;
     h.gmask[0] = window_mask(0, j);
     h.gmask[1] = window_mask(1, j - h.delay);
-    hipError_t e = launch_large_h<T>(h, g.nw, grid, g.lds_h, st);
+    hipError_t e = launch_large_h<T>(h, g.nw, grid, g.lds_h, a.logits != 0, st);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;

@@ -98,6 +98,7 @@ struct ResidentFwdArgs {
   int64_t planes;
   int H, W, dtype;
   int group_h, group_w;  // local-GSPN group lengths (0: global)
+  int logits, renorm;    // w holds Eq. 6 logits (renorm: over on-line neighbours only)
   int use_fixed;   // allow the size-specialised kernel when one exists for H x W
   void* stream;
 };
@@ -120,6 +121,7 @@ struct ResidentBwdArgs {
   int64_t planes;
   int H, W, dtype;
   int group_h, group_w;  // local-GSPN group lengths (0: global)
+  int logits, renorm;    // w holds Eq. 6 logits; dw is the gradient for the logits
   int use_staged;  // allow the LDS-staged kernel for small planes
   void* stream;
 };
@@ -145,6 +147,7 @@ struct LargeFwdArgs {
   int64_t planes;
   int H, W, dtype;
   int group_h, group_w;  // local-GSPN group lengths (0: global)
+  int logits, renorm;    // w holds Eq. 6 logits (renorm: over on-line neighbours only)
   void* stream;
 };
 hipError_t large_fwd_f32(const LargeFwdArgs& a);
@@ -171,6 +174,7 @@ struct LargeBwdHArgs {
   int64_t planes;
   int H, W;
   int group;         // columns per local-GSPN group (0 or >= W: global)
+  int logits, renorm;  // w holds Eq. 6 logits; dw is the gradient for the logits
   void* stream;
 };
 
@@ -188,6 +192,7 @@ struct LargeBwdVArgs {
   int64_t planes;
   int H, W;
   int group;         // rows per local-GSPN group (0: global)
+  int logits, renorm;
   void* stream;
 };
 hipError_t large_bwd_v_rec_f32(const LargeBwdVArgs& a);
@@ -209,6 +214,7 @@ struct LargeBwdVAdjArgs {
   int64_t planes;
   int H, W;
   int group;
+  int logits, renorm;  // w holds Eq. 6 logits; dw is the gradient for the logits
   void* stream;
 };
 hipError_t large_bwd_v_adj_f32(const LargeBwdVAdjArgs& a);

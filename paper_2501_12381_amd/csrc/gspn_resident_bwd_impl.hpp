@@ -66,6 +66,7 @@ struct ResBwdParams {
   // per direction (T2B, B2T, L2R, R2L): bit l set when line l starts a group
   // in that direction's scan order (lines <= 64)
   uint64_t gstart[4];
+  int logits, renorm;  // w holds Eq. 6 logits (dw: their gradient); renorm: on-line neighbours only
 };
 
 // Input ring shared by phase F (x, lam, w0, w1, w2) and phase A (u, dy, w0, w1, w2).
@@ -88,9 +89,10 @@ struct Ring {
 };
 
 // Forward recompute of one direction into its LDS array: h[line][pos].
-template <typename T, int S, bool HZ, bool REV>
+// LG: the weight maps hold Eq. 6 logits, normalised as they are unpacked.
+template <typename T, int S, bool HZ, bool REV, bool LG>
 __device__ __forceinline__ void bwd_forward(const T* const (&pb)[5], float* __restrict__ harr, int sl,
-                                            uint64_t gst) {
+                                            uint64_t gst, bool renorm) {
   using C = BwdCfg<T, S>;
   using RG = Ring<T, S, HZ, REV>;
   constexpr int TL = RG::TL, R = RG::R, NT = RG::NT;
@@ -118,6 +120,7 @@ __device__ __forceinline__ void bwd_forward(const T* const (&pb)[5], float* __re
       const int line = RG::tile_line(ti) + e;
       float xv[1] = {v[0][e]}, lv[1] = {v[1][e]}, a[1] = {v[2][e]}, b[1] = {v[3][e]}, c[1] = {v[4][e]};
       if ((gst >> line) & 1) hp[0] = 0.f;  // local GSPN: a group starts here
+      norm_weights<LG, 1>(a, b, c, sl, S, renorm);
       line_step<1>(xv, lv, a, b, c, vv, hp);
       harr[aoff + (HZ ? line : line * C::P)] = hp[0];
     }
@@ -125,10 +128,11 @@ __device__ __forceinline__ void bwd_forward(const T* const (&pb)[5], float* __re
 }
 
 // Adjoint scan of one direction: reads h from harr, overwrites it with g,
-// writes the direction's three dw maps.
-template <typename T, int S, bool HZ, bool REV>
+// writes the direction's three dw maps (LG: the gradients of the logits,
+// through Eq. 6's Jacobian).
+template <typename T, int S, bool HZ, bool REV, bool LG>
 __device__ __forceinline__ void bwd_adjoint(const T* const (&pb)[5], T* const (&dwp)[3],
-                                            float* __restrict__ harr, int sl, uint64_t gst) {
+                                            float* __restrict__ harr, int sl, uint64_t gst, bool renorm) {
   using C = BwdCfg<T, S>;
   // the adjoint visits lines in the opposite order of the forward scan
   using RG = Ring<T, S, HZ, !REV>;
@@ -173,7 +177,15 @@ __device__ __forceinline__ void bwd_adjoint(const T* const (&pb)[5], T* const (&
       const float hl = from_prev_lane(hpv);
       const float hr = from_next_lane(hpv);
       harr[aoff + (HZ ? line : line * C::P)] = g;
-      const float d0 = g * hl, d1 = g * hpv, d2 = g * hr;
+      float d0 = g * hl, d1 = g * hpv, d2 = g * hr;
+      float c0 = v[2][e], c1 = v[3][e], c2 = v[4][e];
+      if constexpr (LG) {
+        const Norm3 r = normalize3(c0, c1, c2, sl == 0, sl == S - 1, renorm);
+        norm3_vjp(r, d0, d1, d2);
+        c0 = r.w[0];
+        c1 = r.w[1];
+        c2 = r.w[2];
+      }
       if constexpr (HZ) {
         dwb[0][e] = d0; dwb[1][e] = d1; dwb[2][e] = d2;
       } else {
@@ -185,9 +197,9 @@ __device__ __forceinline__ void bwd_adjoint(const T* const (&pb)[5], T* const (&
         }
       }
       gn = g;
-      wn0 = valid ? v[2][e] : 0.f;  // padding lanes hold clamped (foreign) weights
-      wn1 = valid ? v[3][e] : 0.f;
-      wn2 = valid ? v[4][e] : 0.f;
+      wn0 = valid ? c0 : 0.f;  // padding lanes hold clamped (foreign) weights
+      wn1 = valid ? c1 : 0.f;
+      wn2 = valid ? c2 : 0.f;
     }
     if constexpr (HZ) {
       if (valid) {
@@ -226,7 +238,7 @@ __device__ __forceinline__ void bwd_combine(const T* __restrict__ a0, T* __restr
   }
 }
 
-template <typename T, int S>
+template <typename T, int S, bool LG>
 __global__ void __launch_bounds__(256, 2) resident_bwd_kernel(ResBwdParams p) {
   using C = BwdCfg<T, S>;
   constexpr int PPW = C::PPW;
@@ -246,13 +258,14 @@ __global__ void __launch_bounds__(256, 2) resident_bwd_kernel(ResBwdParams p) {
   const int slot = p.slot[wave];
   const T* w0 = slot >= 0 ? (const T*)p.w + (int64_t)slot * 3 * p.npc + plane * HW : nullptr;
   const int64_t pofs = plane * HW;
+  const bool rn = LG && p.renorm;
   if (slot >= 0) {
     const T* pb[5] = {(const T*)p.x + pofs, (const T*)p.lam + pofs, w0, w0 + p.npc, w0 + 2 * p.npc};
     switch (wave) {
-      case 0: bwd_forward<T, S, false, false>(pb, harr, sl, p.gstart[0]); break;
-      case 1: bwd_forward<T, S, false, true>(pb, harr, sl, p.gstart[1]); break;
-      case 2: bwd_forward<T, S, true, false>(pb, harr, sl, p.gstart[2]); break;
-      default: bwd_forward<T, S, true, true>(pb, harr, sl, p.gstart[3]); break;
+      case 0: bwd_forward<T, S, false, false, LG>(pb, harr, sl, p.gstart[0], rn); break;
+      case 1: bwd_forward<T, S, false, true, LG>(pb, harr, sl, p.gstart[1], rn); break;
+      case 2: bwd_forward<T, S, true, false, LG>(pb, harr, sl, p.gstart[2], rn); break;
+      default: bwd_forward<T, S, true, true, LG>(pb, harr, sl, p.gstart[3], rn); break;
     }
   }
   __syncthreads();
@@ -274,10 +287,10 @@ __global__ void __launch_bounds__(256, 2) resident_bwd_kernel(ResBwdParams p) {
     T* dw0 = (T*)p.dw + (int64_t)slot * 3 * p.npc + pofs;
     T* const dwp[3] = {dw0, dw0 + p.npc, dw0 + 2 * p.npc};
     switch (wave) {
-      case 0: bwd_adjoint<T, S, false, false>(pb, dwp, harr, sl, p.gstart[0]); break;
-      case 1: bwd_adjoint<T, S, false, true>(pb, dwp, harr, sl, p.gstart[1]); break;
-      case 2: bwd_adjoint<T, S, true, false>(pb, dwp, harr, sl, p.gstart[2]); break;
-      default: bwd_adjoint<T, S, true, true>(pb, dwp, harr, sl, p.gstart[3]); break;
+      case 0: bwd_adjoint<T, S, false, false, LG>(pb, dwp, harr, sl, p.gstart[0], rn); break;
+      case 1: bwd_adjoint<T, S, false, true, LG>(pb, dwp, harr, sl, p.gstart[1], rn); break;
+      case 2: bwd_adjoint<T, S, true, false, LG>(pb, dwp, harr, sl, p.gstart[2], rn); break;
+      default: bwd_adjoint<T, S, true, true, LG>(pb, dwp, harr, sl, p.gstart[3], rn); break;
     }
   }
   // an absent direction's array stays zero from the initial fill
@@ -304,7 +317,7 @@ inline bool resident_bwd_size_supported(int H, int W) {
 template <typename T, int S>
 hipError_t launch_resident_bwd(const ResBwdParams& p, hipStream_t st) {
   using C = BwdCfg<T, S>;
-  auto kern = resident_bwd_kernel<T, S>;
+  auto kern = p.logits ? resident_bwd_kernel<T, S, true> : resident_bwd_kernel<T, S, false>;
   if (C::LDS_BYTES > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
                                        C::LDS_BYTES);

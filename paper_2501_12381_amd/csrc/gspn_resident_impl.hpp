@@ -90,6 +90,7 @@ struct Phase {
   int W;   // row pitch of the global tensors
   int P;   // row pitch of the LDS accumulator
   int G;   // lines per local-GSPN group (L: the global scan)
+  bool renorm;  // Eq. 6 logits: normalise over the on-line neighbours only
 };
 
 // The five inputs of a line step: x, lam, w0, w1, w2 (pointers at the plane base).
@@ -121,6 +122,24 @@ __device__ __forceinline__ void line_step(const float (&xv)[NP], const float (&l
   }
 #pragma unroll
   for (int q = 0; q < NP; ++q) hp[q] = h[q];
+}
+
+// Eq. 6 on the lane's NP positions (LG: the weight maps hold logits): w0..w2
+// of each position in place, renormalised over on-line neighbours when
+// renorm is set.  Positions past the line keep whatever they get (their h is
+// forced to 0).
+template <bool LG, int NP>
+__device__ __forceinline__ void norm_weights(float (&a)[NP], float (&b)[NP], float (&c)[NP], int pos0, int Pn,
+                                             bool renorm) {
+  if constexpr (LG) {
+#pragma unroll
+    for (int q = 0; q < NP; ++q) {
+      const Norm3 r = normalize3(a[q], b[q], c[q], pos0 + q == 0, pos0 + q == Pn - 1, renorm);
+      a[q] = r.w[0];
+      b[q] = r.w[1];
+      c[q] = r.w[2];
+    }
+  }
 }
 
 // Add h into the accumulator at the step's line.  The value to add to was
@@ -175,7 +194,7 @@ __device__ __forceinline__ void acc_step(float* __restrict__ acc, const int (&of
 // Vertical phase (rows are lines): each lane owns NP contiguous columns.  The
 // five inputs of the next D lines are kept in flight in a register ring: the
 // step that consumes slot k re-issues it for the line D steps ahead.
-template <typename T, bool REV, int NP, int D, bool VV>
+template <typename T, bool REV, int NP, int D, bool VV, bool LG>
 __device__ __forceinline__ void scan_v(const Maps<T>& mp, const Phase& g, float* __restrict__ acc,
                                        int pos0, int pad_off) {
   bool valid[NP];
@@ -236,6 +255,7 @@ __device__ __forceinline__ void scan_v(const Maps<T>& mp, const Phase& g, float*
 #pragma unroll
           for (int q = 0; q < NP; ++q) hp[q] = 0.f;
         }
+        norm_weights<LG, NP>(v[2], v[3], v[4], pos0, g.Pn, g.renorm);
         line_step<NP>(v[0], v[1], v[2], v[3], v[4], valid, hp);
         int off[NP], noff[NP];
 #pragma unroll
@@ -252,7 +272,7 @@ __device__ __forceinline__ void scan_v(const Maps<T>& mp, const Phase& g, float*
 // Horizontal phase (columns are lines): each lane owns NP contiguous rows and
 // reads, per row and map, PD consecutive columns as back-to-back vectors of VL
 // elements (a 32-byte row segment).  Tiles of PD lines are double-buffered.
-template <typename T, bool REV, int NP, int PD, int VL>
+template <typename T, bool REV, int NP, int PD, int VL, bool LG>
 __device__ __forceinline__ void scan_h(const Maps<T>& mp, const Phase& g, float* __restrict__ acc,
                                        int pos0, int pad_off) {
   bool valid[NP];
@@ -305,6 +325,7 @@ __device__ __forceinline__ void scan_h(const Maps<T>& mp, const Phase& g, float*
 #pragma unroll
           for (int q = 0; q < NP; ++q) hp[q] = 0.f;
         }
+        norm_weights<LG, NP>(v[2], v[3], v[4], pos0, g.Pn, g.renorm);
         line_step<NP>(v[0], v[1], v[2], v[3], v[4], valid, hp);
         int off[NP], noff[NP];
 #pragma unroll
@@ -388,9 +409,10 @@ struct ResFwdParams {
   // per direction (T2B, B2T, L2R, R2L): bit l of word l / 64 set when line l
   // (< 128) starts a group in that direction's scan order
   uint64_t gstart[4][2];
+  int logits, renorm;  // w holds Eq. 6 logits (renorm: normalised over on-line neighbours)
 };
 
-template <typename T, int NP, int SEG, int DV, int PDH, bool VV, int VL, int MINW>
+template <typename T, int NP, int SEG, int DV, int PDH, bool VV, int VL, int MINW, bool LG>
 __global__ void __launch_bounds__(128, MINW) resident_fwd_kernel(ResFwdParams p) {
   constexpr int PPW = 64 / SEG;
   extern __shared__ float lds[];
@@ -419,6 +441,7 @@ __global__ void __launch_bounds__(128, MINW) resident_fwd_kernel(ResFwdParams p)
     g.W = p.W;
     g.P = p.P;
     g.G = hz ? p.gw : p.gh;
+    g.renorm = p.renorm != 0;
     if (slot < 0) {
       // the direction is not in the mask: keep the phase's barriers in step
       const int nbar = (g.L & 1) ? 2 : 1;
@@ -429,12 +452,12 @@ __global__ void __launch_bounds__(128, MINW) resident_fwd_kernel(ResFwdParams p)
       mp.m[0] = xb; mp.m[1] = lb; mp.m[2] = w0; mp.m[3] = w0 + p.npc; mp.m[4] = w0 + 2 * p.npc;
       if (!hz) {
         const int pad = p.W;  // padding column (row offset added per step)
-        if (wave == 0) scan_v<T, false, NP, DV, VV>(mp, g, acc, pos0, pad);
-        else scan_v<T, true, NP, DV, VV>(mp, g, acc, pos0, pad);
+        if (wave == 0) scan_v<T, false, NP, DV, VV, LG>(mp, g, acc, pos0, pad);
+        else scan_v<T, true, NP, DV, VV, LG>(mp, g, acc, pos0, pad);
       } else {
         const int pad = p.H * p.P;  // padding row (column added per step)
-        if (wave == 0) scan_h<T, false, NP, PDH, VL>(mp, g, acc, pos0, pad);
-        else scan_h<T, true, NP, PDH, VL>(mp, g, acc, pos0, pad);
+        if (wave == 0) scan_h<T, false, NP, PDH, VL, LG>(mp, g, acc, pos0, pad);
+        else scan_h<T, true, NP, PDH, VL, LG>(mp, g, acc, pos0, pad);
       }
     }
     __syncthreads();
@@ -507,7 +530,8 @@ hipError_t launch_fwd(const ResFwdParams& p, const Config& c, hipStream_t st) {
   constexpr int PDH = (VL == 1 || NP > 2) ? 16 / (int)sizeof(T) / (VL == 1 ? 2 : 1) : 32 / (int)sizeof(T);
   constexpr int MINW = SEG < 64 ? 4 : (NP == 1 ? 2 : 1);
   constexpr int VLc = VL > 16 / (int)sizeof(T) ? 16 / (int)sizeof(T) : VL;
-  auto kern = resident_fwd_kernel<T, NP, SEG, DV, PDH, VV, VLc, MINW>;
+  auto kern = p.logits ? resident_fwd_kernel<T, NP, SEG, DV, PDH, VV, VLc, MINW, true>
+                       : resident_fwd_kernel<T, NP, SEG, DV, PDH, VV, VLc, MINW, false>;
   if (c.lds > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, c.lds);
     if (e != hipSuccess) return e;
@@ -545,6 +569,8 @@ hipError_t resident_fwd_t(const ResidentFwdArgs& a) {
   p.gh = (a.group_h > 0 && a.group_h < a.H) ? a.group_h : a.H;
   p.gw = (a.group_w > 0 && a.group_w < a.W) ? a.group_w : a.W;
   p.grouped = p.gh < a.H || p.gw < a.W;
+  p.logits = a.logits;
+  p.renorm = a.renorm;
   for (int d = 0; d < 4; ++d) {
     const bool hz = d >= 2, rev = d & 1;
     const int L = hz ? a.W : a.H, G = hz ? p.gw : p.gh;
@@ -557,7 +583,7 @@ hipError_t resident_fwd_t(const ResidentFwdArgs& a) {
   p.vec_y = (a.W % v16 == 0 && al(a.u, 16) && al(a.y, 16)) ? 2
           : (a.W % v8 == 0 && al(a.u, 8) && al(a.y, 8)) ? 1 : 0;
   hipStream_t st = (hipStream_t)a.stream;
-  if (a.use_fixed && !p.grouped && a.H == 128 && a.W == 128 && al(a.x, 16) && al(a.lam, 16) && al(a.w, 16) &&
+  if (a.use_fixed && !p.grouped && !p.logits && a.H == 128 && a.W == 128 && al(a.x, 16) && al(a.lam, 16) && al(a.w, 16) &&
       al(a.u, 16) && al(a.y, 16))
     return launch_wide<T>(p, st);  // persistent, every input read once
   if (a.use_fixed && fixed_size_supported(a.H, a.W) && al(a.x, 16) && al(a.lam, 16) && al(a.w, 16)) {

@@ -80,9 +80,10 @@ __device__ __forceinline__ void lds_put2(float* p, float a, float b) { *reinterp
 // One direction's forward recompute from LDS into harr.  harr holds lam * x on
 // entry; each line's entry is read (one pair ahead) before h overwrites it.
 // GRP: local GSPN; bit l of gst is set when line l starts a group.
-template <typename T, int S, bool HZ, bool REV, bool GRP>
+// LG: w holds Eq. 6 logits, normalised as they are read.
+template <typename T, int S, bool HZ, bool REV, bool GRP, bool LG>
 __device__ __forceinline__ void staged_forward(const T* __restrict__ w3, float* __restrict__ harr, int sl,
-                                               bool lane_ok, uint64_t gst) {
+                                               bool lane_ok, uint64_t gst, bool renorm) {
   using C = StagedCfg<T, S>;
   constexpr int NP = S / 2;
   const bool valid = lane_ok && sl < S;
@@ -125,6 +126,15 @@ __device__ __forceinline__ void staged_forward(const T* __restrict__ w3, float* 
 #pragma unroll
       for (int i = 0; i < 4; ++i) cur[t][i] = pre[t][i];
     if (j + 1 < NP) fetch(pre, j + 1);
+    if constexpr (LG) {
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const Norm3 r = normalize3(cur[t][1], cur[t][2], cur[t][3], sl == 0, sl == S - 1, renorm);
+        cur[t][1] = r.w[0];
+        cur[t][2] = r.w[1];
+        cur[t][3] = r.w[2];
+      }
+    }
     float hv[2];
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
@@ -149,10 +159,12 @@ __device__ __forceinline__ void staged_forward(const T* __restrict__ w3, float* 
 // g overwrites h.  Padding lanes (and lanes of absent planes) hold g = 0, so
 // their finite weights (absent planes' are zero-filled) send nothing to a
 // real lane; their stores are skipped.
-template <typename T, int S, bool HZ, bool REV, bool GRP>
+// LG: w holds Eq. 6 logits; dw becomes their gradient (the Jacobian of the
+// normalisation applied per pixel).
+template <typename T, int S, bool HZ, bool REV, bool GRP, bool LG>
 __device__ __forceinline__ void staged_adjoint(const float* __restrict__ udy, T* __restrict__ w3,
                                                float* __restrict__ harr, int sl, bool lane_ok,
-                                               uint64_t gst) {
+                                               uint64_t gst, bool renorm) {
   using C = StagedCfg<T, S>;
   constexpr int NP = S / 2;
   const bool valid = lane_ok && sl < S;
@@ -218,9 +230,17 @@ __device__ __forceinline__ void staged_adjoint(const float* __restrict__ udy, T*
       dv[t][2] = g * from_next_lane(hpv);
       gv[t] = g;
       gn = valid ? g : 0.f;
-      wn0 = cur[t][1];
-      wn1 = cur[t][2];
-      wn2 = cur[t][3];
+      if constexpr (LG) {
+        const Norm3 r = normalize3(cur[t][1], cur[t][2], cur[t][3], sl == 0, sl == S - 1, renorm);
+        norm3_vjp(r, dv[t][0], dv[t][1], dv[t][2]);
+        wn0 = r.w[0];
+        wn1 = r.w[1];
+        wn2 = r.w[2];
+      } else {
+        wn0 = cur[t][1];
+        wn1 = cur[t][2];
+        wn2 = cur[t][3];
+      }
       if constexpr (!HZ) {
         if (valid) {
           const int line = line_of(2 * j + t), e = elem(line);
@@ -253,7 +273,7 @@ __device__ __forceinline__ int staged_aidx(int e0, int r0, int c0, int q) {
 // ND: directions present (compile time, so every index below divides by
 // constants).  Direction arrays are indexed by slot (present directions in
 // increasing direction order), [plane][slot][(S + 1) x (S + 1)].
-template <typename T, int S, int ND, bool GRP>
+template <typename T, int S, int ND, bool GRP, bool LG>
 __global__ void __launch_bounds__(256) staged_bwd_kernel(ResBwdParams p) {
   using C = StagedCfg<T, S>;
   constexpr int PPW = C::PPW, HW = C::HW, NVM = C::NVM, VE = C::VE, MV = C::MV;
@@ -312,6 +332,7 @@ __global__ void __launch_bounds__(256) staged_bwd_kernel(ResBwdParams p) {
   const int sg = seg < PPW ? seg : 0;  // lanes past the group use plane 0's padding
   const int slot = p.slot[wave];
   const int sl0 = slot < 0 ? 0 : slot;
+  const bool rn = LG && p.renorm;
   T* w3 = s_flat + sg * HW + (SM_W + 3 * sl0) * C::MS;
   // u * dy (fp32, written after du) over the u and dy maps: [plane][HW] floats
   float* s_udy = reinterpret_cast<float*>(s_flat + SM_U * C::MS);
@@ -343,10 +364,10 @@ __global__ void __launch_bounds__(256) staged_bwd_kernel(ResBwdParams p) {
 
   if (slot >= 0) {
     switch (wave) {
-      case 0: staged_forward<T, S, false, false, GRP>(w3, harr, sl, lane_ok, p.gstart[0]); break;
-      case 1: staged_forward<T, S, false, true, GRP>(w3, harr, sl, lane_ok, p.gstart[1]); break;
-      case 2: staged_forward<T, S, true, false, GRP>(w3, harr, sl, lane_ok, p.gstart[2]); break;
-      default: staged_forward<T, S, true, true, GRP>(w3, harr, sl, lane_ok, p.gstart[3]); break;
+      case 0: staged_forward<T, S, false, false, GRP, LG>(w3, harr, sl, lane_ok, p.gstart[0], rn); break;
+      case 1: staged_forward<T, S, false, true, GRP, LG>(w3, harr, sl, lane_ok, p.gstart[1], rn); break;
+      case 2: staged_forward<T, S, true, false, GRP, LG>(w3, harr, sl, lane_ok, p.gstart[2], rn); break;
+      default: staged_forward<T, S, true, true, GRP, LG>(w3, harr, sl, lane_ok, p.gstart[3], rn); break;
     }
   }
   lds_barrier();
@@ -380,10 +401,10 @@ __global__ void __launch_bounds__(256) staged_bwd_kernel(ResBwdParams p) {
 
   if (slot >= 0) {
     switch (wave) {
-      case 0: staged_adjoint<T, S, false, false, GRP>(s_udy + sg * HW, w3, harr, sl, lane_ok, p.gstart[0]); break;
-      case 1: staged_adjoint<T, S, false, true, GRP>(s_udy + sg * HW, w3, harr, sl, lane_ok, p.gstart[1]); break;
-      case 2: staged_adjoint<T, S, true, false, GRP>(s_udy + sg * HW, w3, harr, sl, lane_ok, p.gstart[2]); break;
-      default: staged_adjoint<T, S, true, true, GRP>(s_udy + sg * HW, w3, harr, sl, lane_ok, p.gstart[3]); break;
+      case 0: staged_adjoint<T, S, false, false, GRP, LG>(s_udy + sg * HW, w3, harr, sl, lane_ok, p.gstart[0], rn); break;
+      case 1: staged_adjoint<T, S, false, true, GRP, LG>(s_udy + sg * HW, w3, harr, sl, lane_ok, p.gstart[1], rn); break;
+      case 2: staged_adjoint<T, S, true, false, GRP, LG>(s_udy + sg * HW, w3, harr, sl, lane_ok, p.gstart[2], rn); break;
+      default: staged_adjoint<T, S, true, true, GRP, LG>(s_udy + sg * HW, w3, harr, sl, lane_ok, p.gstart[3], rn); break;
     }
     // this direction's three dw maps (written over its w maps by this wave
     // alone) leave at once, while the other waves may still be scanning; the
@@ -444,7 +465,8 @@ template <typename T, int S, int ND>
 hipError_t launch_staged_bwd_nd(const ResBwdParams& p, hipStream_t st) {
   using C = StagedCfg<T, S>;
   constexpr int lds = C::bytes(C::PPW, ND);
-  auto kern = p.grouped ? staged_bwd_kernel<T, S, ND, true> : staged_bwd_kernel<T, S, ND, false>;
+  auto kern = p.logits ? (p.grouped ? staged_bwd_kernel<T, S, ND, true, true> : staged_bwd_kernel<T, S, ND, false, true>)
+                       : (p.grouped ? staged_bwd_kernel<T, S, ND, true, false> : staged_bwd_kernel<T, S, ND, false, false>);
   if (lds > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     if (e != hipSuccess) return e;
@@ -485,6 +507,8 @@ hipError_t resident_bwd_t(const ResidentBwdArgs& a) {
   int n = 0;
   for (int d = 0; d < 4; ++d) p.slot[d] = (a.mask >> d) & 1 ? n++ : -1;
   p.nd = n;
+  p.logits = a.logits;
+  p.renorm = a.renorm;
   const int gh = (a.group_h > 0 && a.group_h < a.H) ? a.group_h : a.H;
   const int gw = (a.group_w > 0 && a.group_w < a.W) ? a.group_w : a.W;
   p.grouped = gh < a.H || gw < a.W;
@@ -501,8 +525,8 @@ hipError_t resident_bwd_t(const ResidentBwdArgs& a) {
   if (!ok || !resident_bwd_size_supported(a.H, a.W)) return hipErrorInvalidValue;
   hipStream_t st = (hipStream_t)a.stream;
   if (a.H == 128) {
-    // persistent 128 x 128 kernel: every pointer 16-byte aligned
-    if (!p.vec) return hipErrorInvalidValue;
+    // persistent 128 x 128 kernel: every pointer 16-byte aligned, plain weights
+    if (!p.vec || p.logits) return hipErrorInvalidValue;
     WideBwdParams q;
     q.dy = a.dy; q.x = a.x; q.lam = a.lam; q.w = a.w; q.u = a.u;
     q.dx = a.dx; q.dw = a.dw; q.dlam = a.dlam; q.du = a.du;

@@ -118,30 +118,6 @@ struct Edges {
   float hi[2][kMaxWaves];  // [parity][wave] value at the wave's last position
 };
 
-// Eq. 6: the three logits of one pixel -> its three weights (sigmoid, then
-// normalised over the neighbours that count: all three, or with edge
-// renormalisation the ones on the line).  Also returns the sigmoids and the
-// normaliser for the Jacobian of the backward.
-struct Norm3 {
-  float w[3], sg[3], m[3], inv;
-};
-__device__ __forceinline__ Norm3 normalize3(float l0, float l1, float l2, bool first_pos, bool last_pos,
-                                            bool renorm) {
-  Norm3 r;
-  r.sg[0] = 1.f / (1.f + __expf(-l0));
-  r.sg[1] = 1.f / (1.f + __expf(-l1));
-  r.sg[2] = 1.f / (1.f + __expf(-l2));
-  r.m[0] = (renorm && first_pos) ? 0.f : 1.f;
-  r.m[1] = 1.f;
-  r.m[2] = (renorm && last_pos) ? 0.f : 1.f;
-  const float s0 = r.m[0] * r.sg[0], s1 = r.sg[1], s2 = r.m[2] * r.sg[2];
-  r.inv = 1.f / (s0 + s1 + s2);
-  r.w[0] = s0 * r.inv;
-  r.w[1] = s1 * r.inv;
-  r.w[2] = s2 * r.inv;
-  return r;
-}
-
 // ---------------------------------------------------------------------------
 // forward pass of one direction
 //   MODE_STORE: acc = h            (ugate: acc = u * h)

@@ -161,6 +161,39 @@ def test_logits_fwd_bwd(shape, dtype, renorm):
         check_bwd(inp, 0xF, algo, dtype, f"logits {shape}", logits=True, renorm=renorm)
 
 
+# shapes that reach each kernel family with logits: size-specialised forward
+# and staged backward (16, 28, 32), per-wave resident backward (56, 64),
+# generic resident forward (128 and ragged), two-pass forward and backward
+# (one band, several bands with halos, ragged last column block)
+LOGIT_FAMILY_SHAPES = [(16, 16), (28, 28), (32, 32), (56, 56), (64, 64), (128, 128), (40, 72), (130, 200),
+                       (600, 136)]
+
+
+@pytest.mark.parametrize("algo", [1, 3, 4], ids=lambda a: ALGO_NAMES[a])
+@pytest.mark.parametrize("renorm", [False, True], ids=["all3", "renorm"])
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16], ids=["f32", "bf16"])
+@pytest.mark.parametrize("shape", LOGIT_FAMILY_SHAPES, ids=lambda s: f"{s[0]}x{s[1]}")
+def test_logits_every_family(shape, dtype, renorm, algo):
+    H, W = shape
+    print(f"[opt] logits family {shape} {dtype} renorm={renorm} {ALGO_NAMES[algo]}", flush=True)
+    planes = 3 if H * W <= 64 * 64 else 1
+    inp = inputs(1, planes, H, W, 0xF, dtype, seed=H * 13 + W + renorm, logits=True)
+    check_fwd(inp, 0xF, algo, dtype, f"logits {shape}", logits=True, renorm=renorm)
+    check_bwd(inp, 0xF, algo, dtype, f"logits {shape}", logits=True, renorm=renorm)
+
+
+@pytest.mark.parametrize("algo", [0, 1, 3, 4], ids=lambda a: ALGO_NAMES[a])
+@pytest.mark.parametrize("case", [(28, 28, 5, 9, 0x5), (64, 64, 16, 5, 0xA), (130, 200, 33, 64, 0xF),
+                                  (600, 136, 100, 7, 0xC)], ids=lambda c: "x".join(map(str, c)))
+def test_logits_with_groups_and_masks(case, algo):
+    H, W, gh, gw, mask = case
+    print(f"[opt] logits groups {case} {ALGO_NAMES[algo]}", flush=True)
+    inp = inputs(1, 2, H, W, mask, torch.float32, seed=H + W + gh + gw, logits=True)
+    opt = dict(group_h=gh, group_w=gw, logits=True, renorm=True)
+    check_fwd(inp, mask, algo, torch.float32, f"logits groups {case}", **opt)
+    check_bwd(inp, mask, algo, torch.float32, f"logits groups {case}", **opt)
+
+
 def test_logits_of_stochastic_weights_match_the_plain_call():
     """Logits with sigmoid(l) = p and sum p = 1 give exactly the plain-weight result."""
     wl = synth.WORKLOADS["cls28_bf16_fb"].with_shape(B=1, C=4, dtype="f32")
