@@ -280,11 +280,6 @@ fixed_fwd_kernel(ResFwdParams p) {
   }
 }
 
-// Sizes with a specialised kernel (square planes).
-inline bool fixed_size_supported(int H, int W) {
-  return H == W && (H == 16 || H == 28 || H == 32 || H == 56 || H == 64);
-}
-
 template <typename T, int S>
 hipError_t launch_fixed(const ResFwdParams& p, hipStream_t st) {
   using C = FixedCfg<T, S>;

@@ -1,0 +1,13 @@
+// Two-pass backward: horizontal adjoint kernels (1 2 3 4 waves), bf16 storage (fp32 arithmetic).
+#include "gspn_large_bwd_impl.hpp"
+
+namespace gspn {
+template hipError_t launch_large_hadj_nw<bf16, 1>(const LargeHAdjParams& p, int dir, int64_t grid, size_t lds, bool lg,
+                                                  hipStream_t st);
+template hipError_t launch_large_hadj_nw<bf16, 2>(const LargeHAdjParams& p, int dir, int64_t grid, size_t lds, bool lg,
+                                                  hipStream_t st);
+template hipError_t launch_large_hadj_nw<bf16, 3>(const LargeHAdjParams& p, int dir, int64_t grid, size_t lds, bool lg,
+                                                  hipStream_t st);
+template hipError_t launch_large_hadj_nw<bf16, 4>(const LargeHAdjParams& p, int dir, int64_t grid, size_t lds, bool lg,
+                                                  hipStream_t st);
+}  // namespace gspn

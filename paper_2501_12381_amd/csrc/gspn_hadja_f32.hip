@@ -1,0 +1,13 @@
+// Two-pass backward: horizontal adjoint kernels (1 2 3 4 waves), fp32.
+#include "gspn_large_bwd_impl.hpp"
+
+namespace gspn {
+template hipError_t launch_large_hadj_nw<float, 1>(const LargeHAdjParams& p, int dir, int64_t grid, size_t lds, bool lg,
+                                                  hipStream_t st);
+template hipError_t launch_large_hadj_nw<float, 2>(const LargeHAdjParams& p, int dir, int64_t grid, size_t lds, bool lg,
+                                                  hipStream_t st);
+template hipError_t launch_large_hadj_nw<float, 3>(const LargeHAdjParams& p, int dir, int64_t grid, size_t lds, bool lg,
+                                                  hipStream_t st);
+template hipError_t launch_large_hadj_nw<float, 4>(const LargeHAdjParams& p, int dir, int64_t grid, size_t lds, bool lg,
+                                                  hipStream_t st);
+}  // namespace gspn

@@ -1,0 +1,7 @@
+// Two-pass backward: horizontal adjoint kernels (8 waves), bf16 storage (fp32 arithmetic).
+#include "gspn_large_bwd_impl.hpp"
+
+namespace gspn {
+template hipError_t launch_large_hadj_nw<bf16, 8>(const LargeHAdjParams& p, int dir, int64_t grid, size_t lds, bool lg,
+                                                  hipStream_t st);
+}  // namespace gspn

@@ -1,13 +1,13 @@
-// Resident-family kernels instantiated for fp32 storage.
+// Resident-family forward dispatch and the generic resident kernels, fp32.
+// The size-specialised and persistent 128 x 128 kernels are instantiated in
+// their own translation units (gspn_fixed_*, gspn_widefwd_*).
 #include "gspn_resident_impl.hpp"
-#include "gspn_fixed_impl.hpp"
-#include "gspn_wide_impl.hpp"
-#include "gspn_staged_bwd_impl.hpp"
 
 namespace gspn {
 hipError_t resident_fwd_f32(const ResidentFwdArgs& a) { return resident_fwd_t<float>(a); }
-hipError_t resident_bwd_f32(const ResidentBwdArgs& a) { return resident_bwd_t<float>(a); }
 }  // namespace gspn
+
+#include "gspn_resident_bwd_impl.hpp"
 
 namespace gspn {
 bool resident_fits(int H, int W, int dtype, bool backward) {

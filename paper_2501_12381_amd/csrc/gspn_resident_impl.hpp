@@ -484,7 +484,10 @@ __global__ void __launch_bounds__(128, MINW) resident_fwd_kernel(ResFwdParams p)
 // host side
 // ---------------------------------------------------------------------------
 namespace gspn {
-inline bool fixed_size_supported(int H, int W);
+// Sizes with a specialised forward kernel (square planes).
+inline bool fixed_size_supported(int H, int W) {
+  return H == W && (H == 16 || H == 28 || H == 32 || H == 56 || H == 64);
+}
 template <typename T, int S> hipError_t launch_fixed(const ResFwdParams& p, hipStream_t st);
 template <typename T> hipError_t launch_wide(const ResFwdParams& p, hipStream_t st);
 namespace resident_detail {
