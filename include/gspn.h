@@ -114,11 +114,9 @@ enum {
 /* Algorithm selection (the `algo` argument).  AUTO picks the fastest kernel
  * family for the shape, groups and flags; the others force one family (for
  * testing), and return GSPN_ERR_UNSUPPORTED when it cannot take the problem.
- * Every family takes groups.  GSPN_FLAG_W_LOGITS and GSPN_FLAG_EDGE_RENORM
- * are taken by every family except the persistent 128 x 128 kernels (AUTO then
- * runs the generic resident forward and the two-pass backward); the
- * per-direction flags by the streaming family only (AUTO routes such a call
- * there). */
+ * Every family takes groups, GSPN_FLAG_W_LOGITS and GSPN_FLAG_EDGE_RENORM;
+ * the per-direction flags are taken by the streaming family only (AUTO routes
+ * such a call there). */
 enum {
   GSPN_ALGO_AUTO = 0,
   GSPN_ALGO_RESIDENT = 1, /* whole plane kept on chip, all directions in one kernel */

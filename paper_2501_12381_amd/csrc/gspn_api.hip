@@ -150,14 +150,12 @@ int check_ws(void* ws, size_t ws_bytes, size_t need,
   return GSPN_OK;
 }
 
-// Eq. 6 logits and edge renormalisation are taken by every family (except the
-// persistent 128 x 128 backward); the per-direction maps by the streaming
-// family only.  Every family takes groups.
+// Eq. 6 logits and edge renormalisation are taken by every family; the
+// per-direction maps by the streaming family only.  Every family takes groups.
 constexpr uint32_t kEq6Flags = GSPN_FLAG_W_LOGITS | GSPN_FLAG_EDGE_RENORM;
 
 bool resident_fits(const Problem& p, int dtype, bool backward) {
   if (p.flags & ~kEq6Flags) return false;
-  if (p.flags && backward && p.H == 128 && p.W == 128) return false;
   if (p.grouped() && !(backward ? kResidentGroupsBwd : kResidentGroupsFwd)) return false;
   return gspn::resident_fits((int)p.H, (int)p.W, dtype, backward);
 }

@@ -586,7 +586,7 @@ hipError_t resident_fwd_t(const ResidentFwdArgs& a) {
   p.vec_y = (a.W % v16 == 0 && al(a.u, 16) && al(a.y, 16)) ? 2
           : (a.W % v8 == 0 && al(a.u, 8) && al(a.y, 8)) ? 1 : 0;
   hipStream_t st = (hipStream_t)a.stream;
-  if (a.use_fixed && !p.grouped && !p.logits && a.H == 128 && a.W == 128 && al(a.x, 16) && al(a.lam, 16) && al(a.w, 16) &&
+  if (a.use_fixed && !p.grouped && a.H == 128 && a.W == 128 && al(a.x, 16) && al(a.lam, 16) && al(a.w, 16) &&
       al(a.u, 16) && al(a.y, 16))
     return launch_wide<T>(p, st);  // persistent, every input read once
   if (a.use_fixed && fixed_size_supported(a.H, a.W) && al(a.x, 16) && al(a.lam, 16) && al(a.w, 16)) {

@@ -525,12 +525,13 @@ hipError_t resident_bwd_t(const ResidentBwdArgs& a) {
   if (!ok || !resident_bwd_size_supported(a.H, a.W)) return hipErrorInvalidValue;
   hipStream_t st = (hipStream_t)a.stream;
   if (a.H == 128) {
-    // persistent 128 x 128 kernel: every pointer 16-byte aligned, plain weights
-    if (!p.vec || p.logits) return hipErrorInvalidValue;
+    // persistent 128 x 128 kernel: every pointer 16-byte aligned
+    if (!p.vec) return hipErrorInvalidValue;
     WideBwdParams q;
     q.dy = a.dy; q.x = a.x; q.lam = a.lam; q.w = a.w; q.u = a.u;
     q.dx = a.dx; q.dw = a.dw; q.dlam = a.dlam; q.du = a.du;
     q.npc = p.npc; q.planes = a.planes;
+    q.logits = a.logits; q.renorm = a.renorm;
     for (int d = 0; d < 4; ++d) q.slot[d] = p.slot[d];
     const int gh = (a.group_h > 0 && a.group_h < 128) ? a.group_h : 128;
     const int gw = (a.group_w > 0 && a.group_w < 128) ? a.group_w : 128;

@@ -125,7 +125,8 @@ constexpr int kWideOob = 0x40000000;
 // planes: the last steps of a plane request the next plane's first rows.
 // PRESENT: the direction is in the mask (otherwise the wave only supplies
 // lam * x and zeros for its first-half rows).
-template <typename T, bool REV, bool PRESENT>
+// LG: the weight maps hold Eq. 6 logits, normalised as they are unpacked.
+template <typename T, bool REV, bool PRESENT, bool LG>
 __device__ __forceinline__ void wide_v_role(const ResFwdParams& p, int slot, float* __restrict__ acc,
                                             float* __restrict__ lxa, int lane) {
   using C = WideCfg<T>;
@@ -135,6 +136,7 @@ __device__ __forceinline__ void wide_v_role(const ResFwdParams& p, int slot, flo
   typedef Pack<T, NP> PK;
   const int col = lane * NP;
   const int voff = col * (int)sizeof(T);
+  const bool rn = LG && p.renorm;
   auto line_of = [](int s) { return REV ? S - 1 - s : s; };
   auto plane_res = [&](int64_t plane, wide_rsrc_t (&rb)[5]) __attribute__((always_inline)) {
     const int64_t pof = plane * (S * S);
@@ -185,6 +187,7 @@ __device__ __forceinline__ void wide_v_role(const ResFwdParams& p, int slot, flo
 #pragma unroll
       for (int q = 0; q < NP; ++q) lxr[s][q] = lx[q];
       if (PRESENT) {
+        norm_weights<LG, NP>(a, b, c, col, S, rn);
         wide_step<NP>(lx, a, b, c, hp);
 #pragma unroll
         for (int q = 0; q < NP; ++q) hr[s][q] = hp[q];
@@ -215,6 +218,7 @@ __device__ __forceinline__ void wide_v_role(const ResFwdParams& p, int slot, flo
       if (s + R < S) load_row(ring[k], rb, s + R, true);
       else load_row(ring[k], rbn, s + R - S, has_next);
       if (s + G < S) lds_read(la[gi], s + G);
+      norm_weights<LG, NP>(a, b, c, col, S, rn);
       wide_step<NP>(lx, a, b, c, hp);
 #pragma unroll
       for (int q = 0; q < NP; ++q) hv[s - MID][q] = hp[q];
@@ -284,7 +288,7 @@ __device__ __forceinline__ void wide_v_role(const ResFwdParams& p, int slot, flo
 // epilogue while they add their second halves (B2-B3); tiles after the
 // second are staggered over the current tile's columns, and the next plane's
 // first tile follows the last one.
-template <typename T, bool REV, bool PRESENT>
+template <typename T, bool REV, bool PRESENT, bool LG>
 __device__ __forceinline__ void wide_h_role(const ResFwdParams& p, int slot, float* __restrict__ acc,
                                             const float* __restrict__ lxa, int lane) {
   using C = WideCfg<T>;
@@ -297,6 +301,7 @@ __device__ __forceinline__ void wide_h_role(const ResFwdParams& p, int slot, flo
   typedef Pack<T, VE> PK;
   typedef Pack<T, NP> UK;
   const int row0 = lane * NP;
+  const bool rn = LG && p.renorm;
   auto tile_so = [](int t) { return (REV ? NTH - 1 - t : t) * TH * (int)sizeof(T); };
   auto plane_res = [&](int64_t plane, wide_rsrc_t (&rw)[3]) __attribute__((always_inline)) {
     const T* w0 = (const T*)p.w + (int64_t)slot * 3 * p.npc + plane * (S * S);
@@ -361,6 +366,7 @@ __device__ __forceinline__ void wide_h_role(const ResFwdParams& p, int slot, flo
         if (i % GAP == 0 && i / GAP < NL) load_seg(tile[1 - b], rw, (i / GAP) / NP, (i / GAP) % NP, tile_so(t + 1));
       }
       if (i + G < TH) lds_read(la[gi], aa[gi], REV ? TH - 1 - (i + G) : i + G);
+      norm_weights<LG, NP>(a, bb, c, row0, S, rn);
       wide_step<NP>(lx, a, bb, c, hp);
 #pragma unroll
       for (int q = 0; q < NP; ++q) acc[(row0 + q) * P + c0 + e] = av[q] + hp[q];
@@ -425,7 +431,7 @@ __device__ __forceinline__ void wide_h_role(const ResFwdParams& p, int slot, flo
   }
 }
 
-template <typename T>
+template <typename T, bool LG>
 __global__ void __launch_bounds__(256, 1) wide_fwd_kernel(ResFwdParams p) {
   using C = WideCfg<T>;
   extern __shared__ float lds[];
@@ -436,20 +442,20 @@ __global__ void __launch_bounds__(256, 1) wide_fwd_kernel(ResFwdParams p) {
   const int slot = p.slot[wave];  // T2B, B2T, L2R, R2L
   switch (wave) {
     case 0:
-      if (slot >= 0) wide_v_role<T, false, true>(p, slot, acc, lxa, lane);
-      else wide_v_role<T, false, false>(p, slot, acc, lxa, lane);
+      if (slot >= 0) wide_v_role<T, false, true, LG>(p, slot, acc, lxa, lane);
+      else wide_v_role<T, false, false, LG>(p, slot, acc, lxa, lane);
       break;
     case 1:
-      if (slot >= 0) wide_v_role<T, true, true>(p, slot, acc, lxa, lane);
-      else wide_v_role<T, true, false>(p, slot, acc, lxa, lane);
+      if (slot >= 0) wide_v_role<T, true, true, LG>(p, slot, acc, lxa, lane);
+      else wide_v_role<T, true, false, LG>(p, slot, acc, lxa, lane);
       break;
     case 2:
-      if (slot >= 0) wide_h_role<T, false, true>(p, slot, acc, lxa, lane);
-      else wide_h_role<T, false, false>(p, slot, acc, lxa, lane);
+      if (slot >= 0) wide_h_role<T, false, true, LG>(p, slot, acc, lxa, lane);
+      else wide_h_role<T, false, false, LG>(p, slot, acc, lxa, lane);
       break;
     default:
-      if (slot >= 0) wide_h_role<T, true, true>(p, slot, acc, lxa, lane);
-      else wide_h_role<T, true, false>(p, slot, acc, lxa, lane);
+      if (slot >= 0) wide_h_role<T, true, true, LG>(p, slot, acc, lxa, lane);
+      else wide_h_role<T, true, false, LG>(p, slot, acc, lxa, lane);
       break;
   }
 }
@@ -471,7 +477,7 @@ inline int wide_cu_count() {
 template <typename T>
 hipError_t launch_wide(const ResFwdParams& p, hipStream_t st) {
   using C = WideCfg<T>;
-  auto kern = wide_fwd_kernel<T>;
+  auto kern = p.logits ? wide_fwd_kernel<T, true> : wide_fwd_kernel<T, false>;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
   if (e != hipSuccess) return e;
   const int64_t cus = wide_cu_count();

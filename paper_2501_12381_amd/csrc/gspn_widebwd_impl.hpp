@@ -74,6 +74,7 @@ struct WideBwdParams {
   // per direction: bit l of word l / 64 set when line l starts a group (the
   // first line of the direction's scan is always set)
   uint64_t gstart[4][2];
+  int logits, renorm;  // w holds Eq. 6 logits (dw: their gradient); renorm: on-line neighbours only
 };
 
 template <int L>
@@ -108,7 +109,9 @@ struct WideBwdRole {
 // ----------------------------------------------------------------------------
 // vertical role: lines are rows, the lane owns columns 2 lane, 2 lane + 1
 // ----------------------------------------------------------------------------
-template <typename T, bool REV>
+// LG: the weight maps hold Eq. 6 logits (normalised as they are unpacked; the
+// adjoint's dw go through the Jacobian before they are stored).
+template <typename T, bool REV, bool LG>
 __device__ __forceinline__ void wb_vertical(const WideBwdParams& p, int64_t plane, int slot, float (&hreg)[128][2],
                                             float* __restrict__ A, const uint64_t (&gst)[2], int lane,
                                             bool forward) {
@@ -122,6 +125,7 @@ __device__ __forceinline__ void wb_vertical(const WideBwdParams& p, int64_t plan
 #pragma unroll
   for (int m = 0; m < 3; ++m) rw[m] = wide_rsrc(w0 + m * p.npc, PB);
   const int voff = 2 * lane * (int)sizeof(T);
+  const bool rn = LG && p.renorm != 0;
   // forward order visits lines fline(0..S-1); the adjoint the reverse
   auto line_at = [&](int s) { return forward ? (REV ? S - 1 - s : s) : (REV ? s : S - 1 - s); };
   PK ring[R][3];
@@ -152,6 +156,7 @@ __device__ __forceinline__ void wb_vertical(const WideBwdParams& p, int64_t plan
       load_row(ring[k], s + R);
       if (s + G < S) RL::lds_get(A, line_at(s + G), lane, la[gi]);
       if (wb_gbit<line>(gst)) hp[0] = hp[1] = 0.f;  // a group starts here
+      norm_weights<LG, NP>(a, b, c, 2 * lane, S, rn);
       wide_step<NP>(lx, a, b, c, hp);
       hreg[line][0] = hp[0];
       hreg[line][1] = hp[1];
@@ -196,13 +201,27 @@ __device__ __forceinline__ void wb_vertical(const WideBwdParams& p, int64_t plan
       float d[3][NP];
       d[0][0] = g[0] * hl0;   d[1][0] = g[0] * hv[0]; d[2][0] = g[0] * hv[1];
       d[0][1] = g[1] * hv[0]; d[1][1] = g[1] * hv[1]; d[2][1] = g[1] * hr1;
+      if constexpr (LG) {
+#pragma unroll
+        for (int q = 0; q < NP; ++q) {
+          const int col = 2 * lane + q;
+          const Norm3 nr = normalize3(ring[k][0].get(q), ring[k][1].get(q), ring[k][2].get(q), col == 0,
+                                      col == S - 1, rn);
+          norm3_vjp(nr, d[0][q], d[1][q], d[2][q]);
+          wn[0][q] = nr.w[0];
+          wn[1][q] = nr.w[1];
+          wn[2][q] = nr.w[2];
+        }
+      }
 #pragma unroll
       for (int m = 0; m < 3; ++m) wide_store<T, NP>(d[m], rd[m], voff, line * RB);
+      if constexpr (!LG) {
 #pragma unroll
-      for (int q = 0; q < NP; ++q) {
-        wn[0][q] = ring[k][0].get(q);
-        wn[1][q] = ring[k][1].get(q);
-        wn[2][q] = ring[k][2].get(q);
+        for (int q = 0; q < NP; ++q) {
+          wn[0][q] = ring[k][0].get(q);
+          wn[1][q] = ring[k][1].get(q);
+          wn[2][q] = ring[k][2].get(q);
+        }
       }
       load_row(ring[k], s + R);
       hreg[line][0] = g[0];
@@ -220,7 +239,7 @@ __device__ __forceinline__ void wb_vertical(const WideBwdParams& p, int64_t plan
 // column groups; the adjoint stages dw in LDS (region `stg`, [map][row][SC]
 // with a 17-word row pitch) and writes it out as 64-byte row segments.
 // ----------------------------------------------------------------------------
-template <typename T, bool REV>
+template <typename T, bool REV, bool LG>
 __device__ __forceinline__ void wb_horizontal(const WideBwdParams& p, int64_t plane, int slot,
                                               float (&hreg)[128][2], float* __restrict__ A,
                                               uint32_t* __restrict__ stg, const uint64_t (&gst)[2], int lane,
@@ -237,6 +256,7 @@ __device__ __forceinline__ void wb_horizontal(const WideBwdParams& p, int64_t pl
   for (int m = 0; m < 3; ++m) rw[m] = wide_rsrc(w0 + m * p.npc, PB);
   const int r0 = 2 * lane;
   const int voff[NP] = {r0 * RB, (r0 + 1) * RB};
+  const bool rn = LG && p.renorm != 0;
   // column-group order: forward visits groups fgrp(0..), the adjoint the reverse
   auto grp_at = [&](int i) { return forward ? (REV ? NGR - 1 - i : i) : (REV ? i : NGR - 1 - i); };
   auto line_at = [&](int s) { return forward ? (REV ? S - 1 - s : s) : (REV ? s : S - 1 - s); };
@@ -271,6 +291,7 @@ __device__ __forceinline__ void wb_horizontal(const WideBwdParams& p, int64_t pl
       if (s % VE == VE - 1) load_grp(ring[k], i + CG);  // the group's last column is read
       if (s + G < S) RL::lds_get(A, line_at(s + G), lane, la[gi]);
       if (wb_gbit<line>(gst)) hp[0] = hp[1] = 0.f;
+      norm_weights<LG, NP>(a, b, c, r0, S, rn);
       wide_step<NP>(lx, a, b, c, hp);
       hreg[line][0] = hp[0];
       hreg[line][1] = hp[1];
@@ -317,16 +338,29 @@ __device__ __forceinline__ void wb_horizontal(const WideBwdParams& p, int64_t pl
       float d[3][NP];
       d[0][0] = g[0] * hl0;   d[1][0] = g[0] * hv[0]; d[2][0] = g[0] * hv[1];
       d[0][1] = g[1] * hv[0]; d[1][1] = g[1] * hv[1]; d[2][1] = g[1] * hr1;
+      if constexpr (LG) {
+#pragma unroll
+        for (int q = 0; q < NP; ++q) {
+          const Norm3 nr = normalize3(ring[k][0][q].get(e), ring[k][1][q].get(e), ring[k][2][q].get(e),
+                                      r0 + q == 0, r0 + q == S - 1, rn);
+          norm3_vjp(nr, d[0][q], d[1][q], d[2][q]);
+          wn[0][q] = nr.w[0];
+          wn[1][q] = nr.w[1];
+          wn[2][q] = nr.w[2];
+        }
+      }
       constexpr int cc = line % SC;  // column inside the staged block
 #pragma unroll
       for (int m = 0; m < 3; ++m)
 #pragma unroll
         for (int q = 0; q < NP; ++q) st[st_idx(m, r0 + q, cc)] = from_f<T>(d[m][q]);
+      if constexpr (!LG) {
 #pragma unroll
-      for (int q = 0; q < NP; ++q) {
-        wn[0][q] = ring[k][0][q].get(e);
-        wn[1][q] = ring[k][1][q].get(e);
-        wn[2][q] = ring[k][2][q].get(e);
+        for (int q = 0; q < NP; ++q) {
+          wn[0][q] = ring[k][0][q].get(e);
+          wn[1][q] = ring[k][1][q].get(e);
+          wn[2][q] = ring[k][2][q].get(e);
+        }
       }
       if (s % VE == VE - 1) load_grp(ring[k], i + CG);
       hreg[line][0] = g[0];
@@ -495,7 +529,7 @@ struct WbRows {
 // The whole per-plane sequence for the wave of direction D (so the state in
 // registers never meets another direction's code at a branch merge).  Every
 // wave executes the same barriers in the same order.
-template <typename T, int D>
+template <typename T, int D, bool LG>
 __device__ __forceinline__ void wide_bwd_wave(const WideBwdParams& p, float* __restrict__ A, float* __restrict__ B,
                                               int lane0) {
   using C = WideBwdCfg<T>;
@@ -520,8 +554,8 @@ __device__ __forceinline__ void wide_bwd_wave(const WideBwdParams& p, float* __r
     // STAMP(2)
     wb_zero_quarter(B, D, lane);  // the sums' array (free until the sum rounds)
     if (present) {
-      if constexpr (HZ) wb_horizontal<T, REV>(p, plane, slot, hreg, A, stg, p.gstart[D], lane, true);
-      else wb_vertical<T, REV>(p, plane, slot, hreg, A, p.gstart[D], lane, true);
+      if constexpr (HZ) wb_horizontal<T, REV, LG>(p, plane, slot, hreg, A, stg, p.gstart[D], lane, true);
+      else wb_vertical<T, REV, LG>(p, plane, slot, hreg, A, p.gstart[D], lane, true);
     }
     int lf = lane;
     asm volatile("" : "+v"(lf));  // keeps the loads below after the scan
@@ -536,8 +570,8 @@ __device__ __forceinline__ void wide_bwd_wave(const WideBwdParams& p, float* __r
     lds_barrier();
     // STAMP(7)
     if (present) {
-      if constexpr (HZ) wb_horizontal<T, REV>(p, plane, slot, hreg, A, stg, p.gstart[D], lane, false);
-      else wb_vertical<T, REV>(p, plane, slot, hreg, A, p.gstart[D], lane, false);
+      if constexpr (HZ) wb_horizontal<T, REV, LG>(p, plane, slot, hreg, A, stg, p.gstart[D], lane, false);
+      else wb_vertical<T, REV, LG>(p, plane, slot, hreg, A, p.gstart[D], lane, false);
     }
     lf = lane;
     asm volatile("" : "+v"(lf));
@@ -556,7 +590,7 @@ __device__ __forceinline__ void wide_bwd_wave(const WideBwdParams& p, float* __r
   }
 }
 
-template <typename T>
+template <typename T, bool LG>
 __global__ void __launch_bounds__(256, 1) wide_bwd_kernel(WideBwdParams p) {
   using C = WideBwdCfg<T>;
   extern __shared__ float lds[];
@@ -564,21 +598,22 @@ __global__ void __launch_bounds__(256, 1) wide_bwd_kernel(WideBwdParams p) {
   float* B = lds + C::ARR;
   const int lane = threadIdx.x & 63;
   switch (__builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6)) {
-    case 0: wide_bwd_wave<T, 0>(p, A, B, lane); break;
-    case 1: wide_bwd_wave<T, 1>(p, A, B, lane); break;
-    case 2: wide_bwd_wave<T, 2>(p, A, B, lane); break;
-    default: wide_bwd_wave<T, 3>(p, A, B, lane); break;
+    case 0: wide_bwd_wave<T, 0, LG>(p, A, B, lane); break;
+    case 1: wide_bwd_wave<T, 1, LG>(p, A, B, lane); break;
+    case 2: wide_bwd_wave<T, 2, LG>(p, A, B, lane); break;
+    default: wide_bwd_wave<T, 3, LG>(p, A, B, lane); break;
   }
 }
 
-// instantiated once per element type (gspn_widebwd_{f32,bf16}.hip)
+// instantiated once per element type and weight kind (gspn_widebwd_*.hip: plain
+// weights and the dispatch; gspn_widebwdlg_*.hip: logits)
 hipError_t wide_bwd_launch_f32(const WideBwdParams& p, hipStream_t st);
 hipError_t wide_bwd_launch_bf16(const WideBwdParams& p, hipStream_t st);
 
-template <typename T>
+template <typename T, bool LG>
 hipError_t launch_wide_bwd(const WideBwdParams& p, hipStream_t st) {
   using C = WideBwdCfg<T>;
-  auto kern = wide_bwd_kernel<T>;
+  auto kern = wide_bwd_kernel<T, LG>;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
   if (e != hipSuccess) return e;
   const int64_t cus = wide_cu_count();
