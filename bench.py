@@ -10,8 +10,9 @@ The headline line measures the largest single-GPU workload: the 4-direction
 bf16 forward on 1 x 320 x 2048 x 2048 planes (an image latent of about 16K
 pixels a side).  Beside it, `extra` holds the other measured workloads (the
 28 x 28 classification-stage forward+backward, the 128 x 128 diffusion-latent
-forward, the 56 x 56 fp32 forward, and forward+backward at both latent
-sizes), each with its own roofline entries.
+forward, the 56 x 56 fp32 forward, forward+backward at both latent sizes, and
+forward+backward at 28 x 28 and 128 x 128 with the paper's Eq. 6 logits
+normalised inside the call), each with its own roofline entries.
 
 Prints one JSON line with the throughput in propagated pixel-channel-directions
 per second (B*C*H*W*n per step / seconds), the roofline position of the
@@ -41,7 +42,8 @@ sys.path.insert(0, ROOT)
 METRIC = "propagated pixel-channel-directions/sec and % of HBM roofline, fwd and fwd+bwd"
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E peak
 DEFAULT_WORKLOAD = "lat2048_bf16"  # the largest workload that fits one GPU
-EXTRA_WORKLOADS = ("cls28_bf16_fb", "lat128_bf16", "cls56_f32", "lat128_bf16_fb", "lat2048_bf16_fb")
+EXTRA_WORKLOADS = ("cls28_bf16_fb", "lat128_bf16", "cls56_f32", "lat128_bf16_fb", "lat2048_bf16_fb",
+                   "cls28_bf16_lg_fb", "lat128_bf16_lg_fb")
 ALGOS = {"auto": 0, "resident": 1, "stream": 2, "resident_generic": 3, "two_pass": 4}
 KERNEL_SRC = os.path.join(ROOT, "paper_2501_12381_amd", "csrc")
 CPU_WORKERS_MAX = 16  # the host-core share of one GPU on the benchmark machines
@@ -166,11 +168,11 @@ def measure(wl, algo: int, bwd_algo: int, steps: int, warmup: int, cold_reps: in
     def step(ev=None):
         if ev is not None:
             ev[0].record()
-        ops.gspn_scan_fwd(x, w, lam, u, wl.mask, algo=algo, y=y)
+        ops.gspn_scan_fwd(x, w, lam, u, wl.mask, algo=algo, y=y, logits=wl.logits)
         if ev is not None:
             ev[1].record()
         if wl.backward:
-            ops.gspn_scan_bwd(inp["dy"], x, w, lam, u, wl.mask, algo=bwd_algo)
+            ops.gspn_scan_bwd(inp["dy"], x, w, lam, u, wl.mask, algo=bwd_algo, logits=wl.logits)
             if ev is not None:
                 ev[2].record()
 
@@ -230,6 +232,7 @@ def measure(wl, algo: int, bwd_algo: int, steps: int, warmup: int, cold_reps: in
     step_bytes = alg_bytes(wl, "fwd") + (alg_bytes(wl, "bwd") if wl.backward else 0)
     r = {"workload": wl.name, "B": wl.B, "C": wl.C, "H": wl.H, "W": wl.W, "mask": wl.mask,
          "directions": wl.n_dirs, "dtype": wl.dtype, "pass": "fwd+bwd" if wl.backward else "fwd",
+         "weights": "eq6_logits" if wl.logits else "normalised",
          "ms_per_step": ms_step, "value": wl.B * wl.C * wl.H * wl.W * wl.n_dirs / (ms_step / 1e3),
          "step_alg_bytes": step_bytes,
          "step_roofline_frac": step_bytes / (ms_step / 1e3) / (HBM_PEAK_GBS * 1e9),

@@ -49,6 +49,7 @@ class Workload:
     backward: bool = False
     seed: int = 0
     extra: dict = field(default_factory=dict)
+    logits: bool = False  # w holds the raw Eq. 6 logits (the call normalises them)
 
     @property
     def n_dirs(self) -> int:
@@ -82,6 +83,10 @@ WORKLOADS = {
 # same inputs, plus dy ~ N(0, 1).
 WORKLOADS["lat128_bf16_fb"] = WORKLOADS["lat128_bf16"].with_shape(name="lat128_bf16_fb", backward=True)
 WORKLOADS["lat2048_bf16_fb"] = WORKLOADS["lat2048_bf16"].with_shape(name="lat2048_bf16_fb", backward=True)
+# The paper's own weights (Eq. 6): the logits go to the call, which normalises
+# them (sigmoid, then the sum over the three neighbours) as it reads them.
+WORKLOADS["cls28_bf16_lg_fb"] = WORKLOADS["cls28_bf16_fb"].with_shape(name="cls28_bf16_lg_fb", logits=True)
+WORKLOADS["lat128_bf16_lg_fb"] = WORKLOADS["lat128_bf16_fb"].with_shape(name="lat128_bf16_lg_fb", logits=True)
 
 
 def torch_dtype(dt: str) -> torch.dtype:
@@ -108,7 +113,8 @@ def _draw(kind: str, shape, device, seed: int, tid: int) -> torch.Tensor:
 
 
 def make_weights(wl: Workload, device="cpu") -> torch.Tensor:
-    """w packed as [n][3][B][C][H][W]: per pixel and direction, softmax of 3 logits."""
+    """w packed as [n][3][B][C][H][W]: per pixel and direction, softmax of 3 logits
+    (or the logits themselves for a workload whose call normalises them)."""
     n = wl.n_dirs
     out = torch.empty((n, 3, wl.B, wl.C, wl.H, wl.W), device=device, dtype=torch_dtype(wl.dtype))
     for di in range(n):  # one direction at a time keeps the fp32 temporaries small
@@ -116,7 +122,7 @@ def make_weights(wl: Workload, device="cpu") -> torch.Tensor:
         logits = torch.randn((3, wl.B, wl.C, wl.H, wl.W), generator=g, device=device,
                              dtype=torch.float32)
         logits.mul_(wl.w_logit_std)
-        out[di].copy_(torch.softmax(logits, dim=0))
+        out[di].copy_(logits if wl.logits else torch.softmax(logits, dim=0))
         del logits
     return out
 

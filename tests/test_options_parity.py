@@ -194,6 +194,32 @@ def test_logits_with_groups_and_masks(case, algo):
     check_bwd(inp, mask, algo, torch.float32, f"logits groups {case}", **opt)
 
 
+@pytest.mark.parametrize("name", ["cls28_bf16_lg_fb", "lat128_bf16_lg_fb"])
+def test_logit_workloads_sampled(name):
+    """The benchmark's logits workloads (full size, AUTO): forward and backward
+    of sampled planes against the oracle with Eq. 6 inside."""
+    wl = synth.WORKLOADS[name]
+    print(f"[opt] workload {name}", flush=True)
+    inp = synth.make_inputs(wl, DEV)
+    y = ops.gspn_scan_fwd(inp["x"], inp["w"], inp["lam"], inp["u"], wl.mask, logits=True)
+    dx, dw, dlam, du = ops.gspn_scan_bwd(inp["dy"], inp["x"], inp["w"], inp["lam"], inp["u"], wl.mask, logits=True)
+    torch.cuda.synchronize()
+    last = (wl.B - 1, wl.C - 1)
+    for b, c in ((0, 0), last):
+        a = {k: np64(v[:, :, b:b + 1, c:c + 1] if k == "w" else v[b:b + 1, c:c + 1]) for k, v in inp.items()}
+        ry = O.scan_fwd(a["x"], a["w"], a["lam"], a["u"], wl.mask, logits=True)
+        assert_close(y[b:b + 1, c:c + 1], ry, torch.bfloat16, f"{name} y ({b},{c})")
+        rdx, rdw, rdlam, rdu = O.scan_bwd(a["dy"], a["x"], a["w"], a["lam"], a["u"], wl.mask, logits=True)
+        assert_close(dx[b:b + 1, c:c + 1], rdx, torch.bfloat16, f"{name} dx ({b},{c})")
+        assert_close(dlam[b:b + 1, c:c + 1], rdlam, torch.bfloat16, f"{name} dlam ({b},{c})")
+        assert_close(du[b:b + 1, c:c + 1], rdu, torch.bfloat16, f"{name} du ({b},{c})")
+        for n in range(rdw.shape[0]):
+            for k in range(3):
+                assert_close(dw[n, k, b:b + 1, c:c + 1], rdw[n, k], torch.bfloat16, f"{name} dw[{n}][{k}] ({b},{c})")
+    del inp, y, dx, dw, dlam, du
+    torch.cuda.empty_cache()
+
+
 def test_logits_of_stochastic_weights_match_the_plain_call():
     """Logits with sigmoid(l) = p and sum p = 1 give exactly the plain-weight result."""
     wl = synth.WORKLOADS["cls28_bf16_fb"].with_shape(B=1, C=4, dtype="f32")
