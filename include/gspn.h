@@ -114,9 +114,11 @@ enum {
 /* Algorithm selection (the `algo` argument).  AUTO picks the fastest kernel
  * family for the shape, groups and flags; the others force one family (for
  * testing), and return GSPN_ERR_UNSUPPORTED when it cannot take the problem.
- * Every family takes groups, GSPN_FLAG_W_LOGITS and GSPN_FLAG_EDGE_RENORM;
- * the per-direction flags are taken by the streaming family only (AUTO routes
- * such a call there). */
+ * Every family takes groups, GSPN_FLAG_W_LOGITS and GSPN_FLAG_EDGE_RENORM.
+ * The per-direction flags are taken by the streaming family, by the resident
+ * family's generic forward (unmerged y, per-direction lam, and per-direction
+ * u with unmerged y) and by its per-wave backward (square planes of 16, 28,
+ * 32, 56 or 64); AUTO picks among those. */
 enum {
   GSPN_ALGO_AUTO = 0,
   GSPN_ALGO_RESIDENT = 1, /* whole plane kept on chip, all directions in one kernel */

@@ -49,17 +49,39 @@ def _run(cmd: list[str]) -> None:
             sys.stderr.write(line + "\n")
 
 
-def build(verbose: bool = False, jobs: int | None = None) -> str:
+def _deps(dep_file: str) -> list[str]:
+    """Files listed in a make-style dependency file written by the compiler."""
+    try:
+        text = open(dep_file).read().replace("\\\n", " ")
+    except OSError:
+        return []
+    _, _, rest = text.partition(":")
+    return rest.split()
+
+
+def _up_to_date(obj: str) -> bool:
+    deps = _deps(obj[:-2] + ".d")
+    if not deps or not os.path.exists(obj):
+        return False
+    t = os.path.getmtime(obj)
+    return all(os.path.exists(d) and os.path.getmtime(d) <= t for d in deps)
+
+
+def build(verbose: bool = False, jobs: int | None = None, incremental: bool = False) -> str:
+    """Compile every unit (incremental: only those whose sources or included
+    headers changed since their object was built) and link libgspn.so."""
     os.makedirs(BUILD, exist_ok=True)
     cc = hipcc()
     srcs = sources()
     objs = [os.path.join(BUILD, os.path.basename(s)[:-4] + ".o") for s in srcs]
-    cmds = [[cc, *FLAGS, "-c", s, "-o", o] for s, o in zip(srcs, objs)]
+    cmds = [[cc, *FLAGS, "-MMD", "-MF", o[:-2] + ".d", "-c", s, "-o", o] for s, o in zip(srcs, objs)
+            if not (incremental and _up_to_date(o))]
     if verbose:
         for c in cmds:
             print(" ".join(c), flush=True)
-    with ThreadPoolExecutor(max_workers=jobs or min(8, len(cmds))) as ex:
-        list(ex.map(_run, cmds))
+    if cmds:
+        with ThreadPoolExecutor(max_workers=jobs or min(8, len(cmds))) as ex:
+            list(ex.map(_run, cmds))
     tmp = LIB + ".tmp"
     link = [cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
     if verbose:
@@ -70,4 +92,4 @@ def build(verbose: bool = False, jobs: int | None = None) -> str:
 
 
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    print(build(verbose="-v" in sys.argv, incremental="--incremental" in sys.argv))

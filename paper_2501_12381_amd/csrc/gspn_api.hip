@@ -151,13 +151,19 @@ int check_ws(void* ws, size_t ws_bytes, size_t need,
 }
 
 // Eq. 6 logits and edge renormalisation are taken by every family; the
-// per-direction maps by the streaming family only.  Every family takes groups.
+// per-direction maps by the generic resident kernels (forward: y_d unmerged,
+// lam_d; u_d only with unmerged outputs), the per-wave resident backward and
+// the streaming family.  Every family takes groups.
 constexpr uint32_t kEq6Flags = GSPN_FLAG_W_LOGITS | GSPN_FLAG_EDGE_RENORM;
+constexpr uint32_t kPdFlags = GSPN_FLAG_LAM_PER_DIR | GSPN_FLAG_U_PER_DIR | GSPN_FLAG_Y_PER_DIR;
 
 bool resident_fits(const Problem& p, int dtype, bool backward) {
-  if (p.flags & ~kEq6Flags) return false;
+  if (p.flags & kPdFlags) {
+    if (!backward && p.u_pd() && !p.y_pd()) return false;
+    if (backward && p.H == 128 && p.W == 128) return false;  // the persistent backward merges
+  }
   if (p.grouped() && !(backward ? kResidentGroupsBwd : kResidentGroupsFwd)) return false;
-  return gspn::resident_fits((int)p.H, (int)p.W, dtype, backward);
+  return gspn::resident_fits((int)p.H, (int)p.W, dtype, backward, (!backward && p.y_pd()) ? p.n : 1);
 }
 
 bool two_pass_fits(const Problem& p, int dtype, bool backward) {
@@ -278,6 +284,7 @@ int gspn_scan_fwd(const void* x, const void* w, const void* lam, const void* u, 
     r.mask = mask; r.planes = p.planes; r.H = (int)H; r.W = (int)W; r.dtype = dtype;
     r.group_h = p.gh; r.group_w = p.gw;
     r.logits = p.logits(); r.renorm = (flags & GSPN_FLAG_EDGE_RENORM) ? 1 : 0;
+    r.lam_pd = p.lam_pd(); r.u_pd = p.u_pd(); r.y_pd = p.y_pd();
     r.use_fixed = a == GSPN_ALGO_RESIDENT;
     r.stream = stream;
     return hip_status(resident_fwd(r));
@@ -376,6 +383,7 @@ int gspn_scan_bwd(const void* dy, const void* x, const void* w, const void* lam,
     r.mask = mask; r.planes = p.planes; r.H = (int)H; r.W = (int)W; r.dtype = dtype;
     r.group_h = p.gh; r.group_w = p.gw;
     r.logits = p.logits(); r.renorm = (flags & GSPN_FLAG_EDGE_RENORM) ? 1 : 0;
+    r.lam_pd = p.lam_pd(); r.u_pd = p.u_pd(); r.y_pd = p.y_pd();
     r.use_staged = a == GSPN_ALGO_RESIDENT;
     r.stream = stream;
     return hip_status(resident_bwd(r));

@@ -99,6 +99,7 @@ struct ResidentFwdArgs {
   int H, W, dtype;
   int group_h, group_w;  // local-GSPN group lengths (0: global)
   int logits, renorm;    // w holds Eq. 6 logits (renorm: over on-line neighbours only)
+  int lam_pd, u_pd, y_pd;  // per-direction maps (generic kernels; u_pd needs y_pd)
   int use_fixed;   // allow the size-specialised kernel when one exists for H x W
   void* stream;
 };
@@ -122,6 +123,7 @@ struct ResidentBwdArgs {
   int H, W, dtype;
   int group_h, group_w;  // local-GSPN group lengths (0: global)
   int logits, renorm;    // w holds Eq. 6 logits; dw is the gradient for the logits
+  int lam_pd, u_pd, y_pd;  // per-direction maps (per-wave resident kernel only)
   int use_staged;  // allow the LDS-staged kernel for small planes
   void* stream;
 };
@@ -130,7 +132,9 @@ hipError_t resident_bwd_bf16(const ResidentBwdArgs& a);
 inline hipError_t resident_bwd(const ResidentBwdArgs& a) {
   return a.dtype == 0 ? resident_bwd_f32(a) : resident_bwd_bf16(a);
 }
-bool resident_fits(int H, int W, int dtype, bool backward);
+// narr: accumulator arrays per plane of the forward (the directions present
+// for unmerged outputs, else 1)
+bool resident_fits(int H, int W, int dtype, bool backward, int narr);
 
 // ---- two-pass family: planes too large for LDS -------------------------------
 struct LargeFwdArgs {

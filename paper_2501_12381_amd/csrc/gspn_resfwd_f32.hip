@@ -10,7 +10,7 @@ hipError_t resident_fwd_f32(const ResidentFwdArgs& a) { return resident_fwd_t<fl
 #include "gspn_resident_bwd_impl.hpp"
 
 namespace gspn {
-bool resident_fits(int H, int W, int dtype, bool backward) {
-  return backward ? resident_bwd_size_supported(H, W) : resident_fwd_fits(H, W, dtype);
+bool resident_fits(int H, int W, int dtype, bool backward, int narr) {
+  return backward ? resident_bwd_size_supported(H, W) : resident_fwd_fits(H, W, dtype, narr);
 }
 }  // namespace gspn

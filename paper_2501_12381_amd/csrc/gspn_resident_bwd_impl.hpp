@@ -67,6 +67,9 @@ struct ResBwdParams {
   // in that direction's scan order (lines <= 64)
   uint64_t gstart[4];
   int logits, renorm;  // w holds Eq. 6 logits (dw: their gradient); renorm: on-line neighbours only
+  // per-direction maps (per-wave kernel only): lam, u, y (and dlam, du, dy)
+  // are (n, B, C, H, W) when set
+  int lam_pd, u_pd, y_pd;
 };
 
 // Input ring shared by phase F (x, lam, w0, w1, w2) and phase A (u, dy, w0, w1, w2).
@@ -238,6 +241,71 @@ __device__ __forceinline__ void bwd_combine(const T* __restrict__ a0, T* __restr
   }
 }
 
+// Per-direction maps: du (or du_d) = sum over the present directions, in
+// order, of dy (or dy_d) * h_d, from the direction arrays of one plane.
+template <typename T, int S, int VE>
+__device__ __forceinline__ void bwd_du_pd(const ResBwdParams& p, int64_t pofs, const float* __restrict__ arr,
+                                          int tid) {
+  using C = BwdCfg<T, S>;
+  constexpr int PR = S / VE;
+  for (int e = tid; e < S * PR; e += 256) {
+    const int r = e / PR, c = (e - r * PR) * VE;
+    const int64_t o = pofs + r * S + c;
+    float acc[VE];
+#pragma unroll
+    for (int q = 0; q < VE; ++q) acc[q] = 0.f;
+    for (int d = 0; d < 4; ++d) {
+      const int s = p.slot[d];
+      if (s < 0) continue;
+      Pack<T, VE> vd;
+      vd.load((const T*)p.dy + (p.y_pd ? s * p.npc : 0) + o);
+      float t[VE];
+#pragma unroll
+      for (int q = 0; q < VE; ++q) t[q] = vd.get(q) * arr[d * C::ARR + r * C::P + c + q];
+      if (p.u_pd) {
+        stv<VE>((T*)p.du + s * p.npc + o, t);
+      } else {
+#pragma unroll
+        for (int q = 0; q < VE; ++q) acc[q] += t[q];
+      }
+    }
+    if (!p.u_pd) stv<VE>((T*)p.du + o, acc);
+  }
+}
+
+// Per-direction lam: dx = sum over the present directions of lam_d g_d, and
+// dlam_d = x g_d.
+template <typename T, int S, int VE>
+__device__ __forceinline__ void bwd_dx_pd(const ResBwdParams& p, int64_t pofs, const float* __restrict__ arr,
+                                          int tid) {
+  using C = BwdCfg<T, S>;
+  constexpr int PR = S / VE;
+  for (int e = tid; e < S * PR; e += 256) {
+    const int r = e / PR, c = (e - r * PR) * VE;
+    const int64_t o = pofs + r * S + c;
+    Pack<T, VE> vx;
+    vx.load((const T*)p.x + o);
+    float acc[VE];
+#pragma unroll
+    for (int q = 0; q < VE; ++q) acc[q] = 0.f;
+    for (int d = 0; d < 4; ++d) {
+      const int s = p.slot[d];
+      if (s < 0) continue;
+      Pack<T, VE> vl;
+      vl.load((const T*)p.lam + s * p.npc + o);
+      float t[VE];
+#pragma unroll
+      for (int q = 0; q < VE; ++q) {
+        const float g = arr[d * C::ARR + r * C::P + c + q];
+        acc[q] += vl.get(q) * g;
+        t[q] = vx.get(q) * g;
+      }
+      stv<VE>((T*)p.dlam + s * p.npc + o, t);
+    }
+    stv<VE>((T*)p.dx + o, acc);
+  }
+}
+
 template <typename T, int S, bool LG>
 __global__ void __launch_bounds__(256, 2) resident_bwd_kernel(ResBwdParams p) {
   using C = BwdCfg<T, S>;
@@ -260,7 +328,8 @@ __global__ void __launch_bounds__(256, 2) resident_bwd_kernel(ResBwdParams p) {
   const int64_t pofs = plane * HW;
   const bool rn = LG && p.renorm;
   if (slot >= 0) {
-    const T* pb[5] = {(const T*)p.x + pofs, (const T*)p.lam + pofs, w0, w0 + p.npc, w0 + 2 * p.npc};
+    const T* pb[5] = {(const T*)p.x + pofs, (const T*)p.lam + (p.lam_pd ? slot * p.npc : 0) + pofs, w0,
+                      w0 + p.npc, w0 + 2 * p.npc};
     switch (wave) {
       case 0: bwd_forward<T, S, false, false, LG>(pb, harr, sl, p.gstart[0], rn); break;
       case 1: bwd_forward<T, S, false, true, LG>(pb, harr, sl, p.gstart[1], rn); break;
@@ -270,11 +339,16 @@ __global__ void __launch_bounds__(256, 2) resident_bwd_kernel(ResBwdParams p) {
   }
   __syncthreads();
 
-  // du = dy * sum_d h_d
+  // du = dy * sum_d h_d (per-direction maps: the sum of dy_d h_d, or du_d)
   for (int pl = 0; pl < PPW; ++pl) {
     const int64_t pi = g0 + pl;
     if (pi >= p.planes) break;
     const float* arr = lds + pl * 4 * C::ARR;
+    if (p.u_pd || p.y_pd) {
+      if (p.vec) bwd_du_pd<T, S, C::VE>(p, pi * HW, arr, tid);
+      else bwd_du_pd<T, S, 1>(p, pi * HW, arr, tid);
+      continue;
+    }
     const T* dyb = (const T*)p.dy + pi * HW;
     T* dub = (T*)p.du + pi * HW;
     if (p.vec) bwd_combine<T, S, C::VE>(dyb, dub, nullptr, nullptr, arr, tid);
@@ -283,7 +357,8 @@ __global__ void __launch_bounds__(256, 2) resident_bwd_kernel(ResBwdParams p) {
   __syncthreads();
 
   if (slot >= 0) {
-    const T* pb[5] = {(const T*)p.u + pofs, (const T*)p.dy + pofs, w0, w0 + p.npc, w0 + 2 * p.npc};
+    const T* pb[5] = {(const T*)p.u + (p.u_pd ? slot * p.npc : 0) + pofs,
+                      (const T*)p.dy + (p.y_pd ? slot * p.npc : 0) + pofs, w0, w0 + p.npc, w0 + 2 * p.npc};
     T* dw0 = (T*)p.dw + (int64_t)slot * 3 * p.npc + pofs;
     T* const dwp[3] = {dw0, dw0 + p.npc, dw0 + 2 * p.npc};
     switch (wave) {
@@ -302,6 +377,11 @@ __global__ void __launch_bounds__(256, 2) resident_bwd_kernel(ResBwdParams p) {
     if (pi >= p.planes) break;
     const float* arr = lds + pl * 4 * C::ARR;
     const int64_t o = pi * HW;
+    if (p.lam_pd) {
+      if (p.vec) bwd_dx_pd<T, S, C::VE>(p, o, arr, tid);
+      else bwd_dx_pd<T, S, 1>(p, o, arr, tid);
+      continue;
+    }
     if (p.vec)
       bwd_combine<T, S, C::VE>(
           (const T*)p.lam + o, (T*)p.dx + o, (const T*)p.x + o, (T*)p.dlam + o, arr, tid);

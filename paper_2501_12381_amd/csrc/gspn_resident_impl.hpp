@@ -393,6 +393,28 @@ __device__ __forceinline__ void epilogue(const T* __restrict__ ub, T* __restrict
   }
 }
 
+// Unmerged outputs: y_d = u_d * acc_d for the n directions of one plane in one
+// pass (u read once when it is shared), acc_d at ac + d * accsz.
+template <typename T, int VE>
+__device__ __forceinline__ void epilogue_pd(const T* __restrict__ ub, int64_t ustride, T* __restrict__ yb,
+                                            int64_t ystride, const float* __restrict__ ac, int accsz, int n,
+                                            int H, int W, int P, int tid) {
+  const int per_row = W / VE;
+  const int cnt = H * per_row;
+  for (int e = tid; e < cnt; e += 128) {
+    const int r = e / per_row, c = (e - r * per_row) * VE;
+    Pack<T, VE> uv;
+    uv.load(ub + (int64_t)r * W + c);
+    for (int d = 0; d < n; ++d) {
+      if (d > 0 && ustride) uv.load(ub + d * ustride + (int64_t)r * W + c);
+      float yv[VE];
+#pragma unroll
+      for (int q = 0; q < VE; ++q) yv[q] = uv.get(q) * ac[d * accsz + r * P + c + q];
+      stv<VE>(yb + d * ystride + (int64_t)r * W + c, yv);
+    }
+  }
+}
+
 struct ResFwdParams {
   const void* x;
   const void* lam;
@@ -410,6 +432,11 @@ struct ResFwdParams {
   // (< 128) starts a group in that direction's scan order
   uint64_t gstart[4][2];
   int logits, renorm;  // w holds Eq. 6 logits (renorm: normalised over on-line neighbours)
+  // per-direction maps (generic kernel only): lam_pd: lam is (n, B, C, H, W);
+  // y_pd: y is (n, B, C, H, W), y_d = u_d h_d, one LDS array per direction;
+  // u_pd (with y_pd): u is (n, B, C, H, W)
+  int lam_pd, u_pd, y_pd;
+  int nd;              // directions present
 };
 
 template <typename T, int NP, int SEG, int DV, int PDH, bool VV, int VL, int MINW, bool LG>
@@ -422,14 +449,13 @@ __global__ void __launch_bounds__(128, MINW) resident_fwd_kernel(ResFwdParams p)
   const int64_t plane = (g0 + seg < p.planes) ? g0 + seg : p.planes - 1;  // clamp: stores are skipped
   const int64_t HW = (int64_t)p.H * p.W;
   const int accsz = (p.H + 1) * p.P;
+  const int narr = p.y_pd ? p.nd : 1;  // accumulator arrays per plane
 
-  for (int e = tid; e < PPW * accsz; e += 128) lds[e] = 0.f;
+  for (int e = tid; e < PPW * narr * accsz; e += 128) lds[e] = 0.f;
   __syncthreads();
 
-  float* acc = lds + seg * accsz;
   const int pos0 = sl * NP;
   const T* xb = (const T*)p.x + plane * HW;
-  const T* lb = (const T*)p.lam + plane * HW;
 
 #pragma unroll
   for (int ph = 0; ph < 2; ++ph) {
@@ -448,6 +474,9 @@ __global__ void __launch_bounds__(128, MINW) resident_fwd_kernel(ResFwdParams p)
       for (int b = 0; b < nbar; ++b) lds_barrier();
     } else {
       const T* w0 = (const T*)p.w + (int64_t)slot * 3 * p.npc + plane * HW;
+      const T* lb = (const T*)p.lam + (p.lam_pd ? slot * p.npc : 0) + plane * HW;
+      // the direction's own array (unmerged outputs) or the shared accumulator
+      float* acc = lds + (seg * narr + (p.y_pd ? slot : 0)) * accsz;
       Maps<T> mp;
       mp.m[0] = xb; mp.m[1] = lb; mp.m[2] = w0; mp.m[3] = w0 + p.npc; mp.m[4] = w0 + 2 * p.npc;
       if (!hz) {
@@ -471,7 +500,14 @@ __global__ void __launch_bounds__(128, MINW) resident_fwd_kernel(ResFwdParams p)
     if (pi >= p.planes) break;
     const T* ub = (const T*)p.u + pi * HW;
     T* yb = (T*)p.y + pi * HW;
-    const float* ac = lds + pl * accsz;
+    const float* ac = lds + pl * narr * accsz;
+    if (p.y_pd) {
+      const int64_t us = p.u_pd ? p.npc : 0;
+      if (p.vec_y == 2) epilogue_pd<T, 16 / sizeof(T)>(ub, us, yb, p.npc, ac, accsz, narr, p.H, p.W, p.P, tid);
+      else if (p.vec_y == 1) epilogue_pd<T, 8 / sizeof(T)>(ub, us, yb, p.npc, ac, accsz, narr, p.H, p.W, p.P, tid);
+      else epilogue_pd<T, 1>(ub, us, yb, p.npc, ac, accsz, narr, p.H, p.W, p.P, tid);
+      continue;
+    }
     if (p.vec_y == 2) epilogue<T, 16 / sizeof(T)>(ub, yb, ac, p.H, p.W, p.P, tid);
     else if (p.vec_y == 1) epilogue<T, 8 / sizeof(T)>(ub, yb, ac, p.H, p.W, p.P, tid);
     else epilogue<T, 1>(ub, yb, ac, p.H, p.W, p.P, tid);
@@ -502,13 +538,14 @@ struct Config {
 
 inline bool al(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
-inline bool config_for(int H, int W, size_t es, const void* const* ptrs, int nptr, Config* c) {
+// narr: accumulator arrays per plane (one per direction for unmerged outputs)
+inline bool config_for(int H, int W, size_t es, const void* const* ptrs, int nptr, Config* c, int narr = 1) {
   const int mx = H > W ? H : W;
   if (mx > kMaxLine) return false;
   c->np = mx <= 64 ? 1 : (mx <= 128 ? 2 : 4);
   c->seg = mx <= 15 ? 16 : (mx <= 31 ? 32 : 64);
   c->P = W + 1 + (W & 1);
-  const long lds = (long)(64 / c->seg) * (H + 1) * c->P * 4;
+  const long lds = (long)(64 / c->seg) * narr * (H + 1) * c->P * 4;
   if (lds > kMaxLds) return false;
   c->lds = (int)lds;
   auto ptrs_al = [&](int n_el) {
@@ -560,15 +597,21 @@ template <typename T>
 hipError_t resident_fwd_t(const ResidentFwdArgs& a) {
   using namespace resident_detail;
   const void* ptrs[] = {a.x, a.lam, a.w};
+  int n = 0;
+  for (int d = 0; d < 4; ++d) n += (a.mask >> d) & 1;
+  const bool pd = a.lam_pd || a.u_pd || a.y_pd;
+  if (a.u_pd && !a.y_pd) return hipErrorInvalidValue;  // a merged y with per-direction u: streaming family
   Config c;
-  if (!config_for(a.H, a.W, sizeof(T), ptrs, 3, &c)) return hipErrorInvalidValue;
+  if (!config_for(a.H, a.W, sizeof(T), ptrs, 3, &c, a.y_pd ? n : 1)) return hipErrorInvalidValue;
   ResFwdParams p;
   p.x = a.x; p.lam = a.lam; p.w = a.w; p.u = a.u; p.y = a.y;
   p.npc = (int64_t)a.planes * a.H * a.W;
   p.planes = a.planes;
   p.H = a.H; p.W = a.W; p.P = c.P;
-  int n = 0;
+  n = 0;
   for (int d = 0; d < 4; ++d) p.slot[d] = (a.mask >> d) & 1 ? n++ : -1;
+  p.nd = n;
+  p.lam_pd = a.lam_pd; p.u_pd = a.u_pd; p.y_pd = a.y_pd;
   p.gh = (a.group_h > 0 && a.group_h < a.H) ? a.group_h : a.H;
   p.gw = (a.group_w > 0 && a.group_w < a.W) ? a.group_w : a.W;
   p.grouped = p.gh < a.H || p.gw < a.W;
@@ -583,13 +626,16 @@ hipError_t resident_fwd_t(const ResidentFwdArgs& a) {
   }
   // epilogue vectors: 16 bytes if rows allow, else 8 bytes, else scalars
   const int v16 = 16 / (int)sizeof(T), v8 = 8 / (int)sizeof(T);
-  p.vec_y = (a.W % v16 == 0 && al(a.u, 16) && al(a.y, 16)) ? 2
-          : (a.W % v8 == 0 && al(a.u, 8) && al(a.y, 8)) ? 1 : 0;
+  // per-direction maps start npc elements apart: their starts must keep the alignment too
+  const size_t mapb = (size_t)p.npc * sizeof(T);
+  p.vec_y = (a.W % v16 == 0 && al(a.u, 16) && al(a.y, 16) && (!pd || mapb % 16 == 0)) ? 2
+          : (a.W % v8 == 0 && al(a.u, 8) && al(a.y, 8) && (!pd || mapb % 8 == 0)) ? 1 : 0;
   hipStream_t st = (hipStream_t)a.stream;
-  if (a.use_fixed && !p.grouped && a.H == 128 && a.W == 128 && al(a.x, 16) && al(a.lam, 16) && al(a.w, 16) &&
-      al(a.u, 16) && al(a.y, 16))
+  // per-direction maps run on the generic kernels only
+  if (!pd && a.use_fixed && !p.grouped && a.H == 128 && a.W == 128 && al(a.x, 16) && al(a.lam, 16) &&
+      al(a.w, 16) && al(a.u, 16) && al(a.y, 16))
     return launch_wide<T>(p, st);  // persistent, every input read once
-  if (a.use_fixed && fixed_size_supported(a.H, a.W) && al(a.x, 16) && al(a.lam, 16) && al(a.w, 16)) {
+  if (!pd && a.use_fixed && fixed_size_supported(a.H, a.W) && al(a.x, 16) && al(a.lam, 16) && al(a.w, 16)) {
     switch (a.H) {
       case 16: return launch_fixed<T, 16>(p, st);
       case 28: return launch_fixed<T, 28>(p, st);
@@ -605,9 +651,10 @@ hipError_t resident_fwd_t(const ResidentFwdArgs& a) {
   return c.vv ? launch_fwd_vl<T, 4, 64, true>(p, c, st) : launch_fwd_vl<T, 4, 64, false>(p, c, st);
 }
 
-inline bool resident_fwd_fits(int H, int W, int dtype) {
+// narr: accumulator arrays per plane (the directions present, for unmerged outputs)
+inline bool resident_fwd_fits(int H, int W, int dtype, int narr = 1) {
   resident_detail::Config c;
-  return resident_detail::config_for(H, W, dtype == 0 ? 4 : 2, nullptr, 0, &c);
+  return resident_detail::config_for(H, W, dtype == 0 ? 4 : 2, nullptr, 0, &c, narr);
 }
 
 }  // namespace gspn

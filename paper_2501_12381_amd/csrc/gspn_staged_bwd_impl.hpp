@@ -509,6 +509,8 @@ hipError_t resident_bwd_t(const ResidentBwdArgs& a) {
   p.nd = n;
   p.logits = a.logits;
   p.renorm = a.renorm;
+  p.lam_pd = a.lam_pd; p.u_pd = a.u_pd; p.y_pd = a.y_pd;
+  const bool pd = a.lam_pd || a.u_pd || a.y_pd;
   const int gh = (a.group_h > 0 && a.group_h < a.H) ? a.group_h : a.H;
   const int gw = (a.group_w > 0 && a.group_w < a.W) ? a.group_w : a.W;
   p.grouped = gh < a.H || gw < a.W;
@@ -525,8 +527,8 @@ hipError_t resident_bwd_t(const ResidentBwdArgs& a) {
   if (!ok || !resident_bwd_size_supported(a.H, a.W)) return hipErrorInvalidValue;
   hipStream_t st = (hipStream_t)a.stream;
   if (a.H == 128) {
-    // persistent 128 x 128 kernel: every pointer 16-byte aligned
-    if (!p.vec) return hipErrorInvalidValue;
+    // persistent 128 x 128 kernel: every pointer 16-byte aligned, merged maps
+    if (!p.vec || pd) return hipErrorInvalidValue;
     WideBwdParams q;
     q.dy = a.dy; q.x = a.x; q.lam = a.lam; q.w = a.w; q.u = a.u;
     q.dx = a.dx; q.dw = a.dw; q.dlam = a.dlam; q.du = a.du;
@@ -544,7 +546,7 @@ hipError_t resident_bwd_t(const ResidentBwdArgs& a) {
     }
     return sizeof(T) == 4 ? wide_bwd_launch_f32(q, st) : wide_bwd_launch_bf16(q, st);
   }
-  if (a.use_staged && p.vec && staged_bwd_size_supported<T>(a.H, a.W))
+  if (a.use_staged && p.vec && !pd && staged_bwd_size_supported<T>(a.H, a.W))
     return launch_staged_bwd_size<T>(p, a.H, st);
   switch (a.H) {
     case 16: return launch_resident_bwd<T, 16>(p, st);

@@ -251,6 +251,28 @@ def test_per_direction_maps(mask, dtype, pd):
     check_bwd(inp, mask, 0, dtype, f"per-dir {pd}", **opt)
 
 
+# square planes that the per-wave resident backward takes, and a ragged one
+# for the generic resident forward (its backward streams)
+PD_SHAPES = [(16, 16), (28, 28), (56, 56), (64, 64), (40, 72)]
+
+
+@pytest.mark.parametrize("algo", [0, 1, 3], ids=lambda a: ALGO_NAMES[a])
+@pytest.mark.parametrize("pd", PD, ids=lambda p: "".join("LUY"[i] if f else "-" for i, f in enumerate(p)))
+@pytest.mark.parametrize("shape", PD_SHAPES, ids=lambda s: f"{s[0]}x{s[1]}")
+def test_per_direction_maps_resident(shape, pd, algo):
+    """Per-direction maps on the resident families (forced and AUTO), with
+    logits, against the oracle."""
+    H, W = shape
+    lpd, upd, ypd = pd
+    print(f"[opt] per-direction resident {shape} {pd} {ALGO_NAMES[algo]}", flush=True)
+    mask = 0xB
+    inp = inputs(1, 3, H, W, mask, torch.bfloat16, seed=H + W + sum(pd), lam_pd=lpd, u_pd=upd, y_pd=ypd,
+                 logits=True)
+    opt = dict(lam_per_dir=lpd, u_per_dir=upd, y_per_dir=ypd, logits=True)
+    check_fwd(inp, mask, algo, torch.bfloat16, f"per-dir {shape} {pd}", **opt)
+    check_bwd(inp, mask, algo, torch.bfloat16, f"per-dir {shape} {pd}", **opt)
+
+
 def test_all_options_together_autograd():
     """Groups, logits with edge renormalisation and per-direction maps through
     the autograd wrapper."""
