@@ -118,7 +118,8 @@ enum {
  * The per-direction flags are taken by the streaming family, by the resident
  * family's generic forward (unmerged y, per-direction lam, and per-direction
  * u with unmerged y) and by its per-wave backward (square planes of 16, 28,
- * 32, 56 or 64); AUTO picks among those. */
+ * 32, 56 or 64); GSPN_FLAG_Y_PER_DIR alone also by the two-pass family.  AUTO
+ * picks among those. */
 enum {
   GSPN_ALGO_AUTO = 0,
   GSPN_ALGO_RESIDENT = 1, /* whole plane kept on chip, all directions in one kernel */
@@ -136,6 +137,9 @@ enum {
                             recompute their h in one pass and run both adjoints in
                             another.  Workspace: three fp32 B*C*H*W arrays (four
                             with both vertical directions) and 6*B*C*H floats.
+                            Unmerged outputs (GSPN_FLAG_Y_PER_DIR): the forward
+                            writes each direction's y and needs only the column
+                            state; the backward seeds each direction from its dy.
                             Needs W * element size a multiple of 16 bytes and at
                             least 128 bytes, W <= 4096 (bf16) or 2048 (f32), and
                             16-byte aligned tensors (AUTO falls back to streaming). */

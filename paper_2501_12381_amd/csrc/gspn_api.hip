@@ -166,8 +166,10 @@ bool resident_fits(const Problem& p, int dtype, bool backward) {
   return gspn::resident_fits((int)p.H, (int)p.W, dtype, backward, (!backward && p.y_pd()) ? p.n : 1);
 }
 
+// the two-pass family takes unmerged outputs (per-direction y and dy) but not
+// per-direction lam or u
 bool two_pass_fits(const Problem& p, int dtype, bool backward) {
-  if ((p.flags & ~kEq6Flags) || (p.grouped() && !kTwoPassGroups)) return false;
+  if ((p.flags & ~(kEq6Flags | GSPN_FLAG_Y_PER_DIR)) || (p.grouped() && !kTwoPassGroups)) return false;
   // the backward runs its horizontal directions on the two-pass kernels
   // (their vertical ones on the streaming kernels)
   if (backward && !(p.mask & (DIR_L2R | DIR_R2L))) return false;
@@ -200,7 +202,8 @@ size_t two_pass_state_bytes(const Problem& p, uint32_t mask) {
 
 size_t fwd_ws_bytes(const Problem& p, int algo, uint32_t mask) {
   if (algo == GSPN_ALGO_STREAM && p.n > 1 && !p.y_pd()) return round_up((size_t)p.npc * 4, kWsAlign);
-  if (algo == GSPN_ALGO_TWO_PASS) return two_pass_acc_bytes(p, mask) + two_pass_state_bytes(p, mask);
+  if (algo == GSPN_ALGO_TWO_PASS)
+    return (p.y_pd() ? 0 : two_pass_acc_bytes(p, mask)) + two_pass_state_bytes(p, mask);
   return 0;
 }
 
@@ -292,9 +295,12 @@ int gspn_scan_fwd(const void* x, const void* w, const void* lam, const void* u, 
   if (a == GSPN_ALGO_TWO_PASS) {
     LargeFwdArgs l{};
     l.x = x; l.lam = lam; l.w = w; l.u = u; l.y = y;
-    l.acc = (float*)workspace;
-    l.acc_b = two_pass_split_v(mask) ? (float*)((char*)workspace + round_up((size_t)p.npc * 4, kWsAlign)) : nullptr;
-    l.state = (float*)((char*)workspace + two_pass_acc_bytes(p, mask));
+    const size_t accb = p.y_pd() ? 0 : two_pass_acc_bytes(p, mask);
+    l.acc = p.y_pd() ? nullptr : (float*)workspace;
+    l.acc_b = (!p.y_pd() && two_pass_split_v(mask))
+                  ? (float*)((char*)workspace + round_up((size_t)p.npc * 4, kWsAlign)) : nullptr;
+    l.state = (float*)((char*)workspace + accb);
+    l.y_pd = p.y_pd();
     l.mask = mask; l.planes = p.planes; l.H = (int)H; l.W = (int)W; l.dtype = dtype;
     l.group_h = p.gh; l.group_w = p.gw;
     l.logits = p.logits(); l.renorm = (flags & GSPN_FLAG_EDGE_RENORM) ? 1 : 0;
@@ -405,7 +411,9 @@ int gspn_scan_bwd(const void* dy, const void* x, const void* w, const void* lam,
     for (int d = 2; d < 4; ++d) {
       if (slot[d] < 0) continue;
       LargeBwdHArgs l{};
-      l.x = x; l.lam = lam; l.dy = dy; l.u = u;
+      l.x = x; l.lam = lam; l.u = u;
+      l.dy = (const char*)dy + (p.y_pd() ? (size_t)slot[d] * tb : 0);
+      l.hdy = p.y_pd() ? l.dy : nullptr;
       l.w = (const char*)w + (size_t)slot[d] * 3 * tb;
       l.dw = (char*)dw + (size_t)slot[d] * 3 * tb;
       l.hbuf = hprev; l.hsum = hsum; l.gsum = gsum; l.state = state;
@@ -443,6 +451,7 @@ int gspn_scan_bwd(const void* dy, const void* x, const void* w, const void* lam,
       r.planes = p.planes; r.H = (int)H; r.W = (int)W;
       r.group = p.gh;
       r.logits = p.logits(); r.renorm = (flags & GSPN_FLAG_EDGE_RENORM) ? 1 : 0;
+      r.y_pd = p.y_pd();
       r.stream = stream;
       st = hip_status(large_bwd_v_adj(r, dtype));
       if (st != GSPN_OK) return st;
@@ -450,6 +459,13 @@ int gspn_scan_bwd(const void* dy, const void* x, const void* w, const void* lam,
     GradFinishArgs g{};
     g.x = x; g.lam = lam; g.dy = dy; g.gsum = gsum; g.hsum = hsum; g.hsum2 = hv[0] ? hv[0] : hv[1];
     g.hsum3 = hv[0] ? hv[1] : nullptr;
+    if (p.y_pd()) {
+      // unmerged outputs: du = sum_d dy_d h_d (the horizontal part is in hsum)
+      const int s2 = hv[0] ? slot[0] : slot[1], s3 = hv[0] ? slot[1] : -1;
+      g.du_mode = 3;
+      g.dy2 = s2 >= 0 ? (const char*)dy + (size_t)s2 * tb : nullptr;
+      g.dy3 = s3 >= 0 ? (const char*)dy + (size_t)s3 * tb : nullptr;
+    }
     g.dx = dx; g.dlam = dlam; g.du = du; g.n = p.npc; g.dtype = dtype;
     g.stream = stream;
     return hip_status(grad_finish(g));

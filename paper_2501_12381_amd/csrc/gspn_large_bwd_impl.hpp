@@ -337,6 +337,7 @@ hipError_t large_bwd_h_t(const LargeBwdHArgs& a) {
   h.rec = 1;
   h.hbuf = a.hbuf;
   h.renorm = a.renorm;
+  h.hdy = a.hdy;
   for (int j = 0; j < g.nblk; ++j) {
     const int blk = a.dir ? g.nblk - 1 - j : j;
     const int ws = window(blk);
@@ -428,6 +429,7 @@ struct LargeVAdjParams {
   int slot[2];          // weight slots of top-to-bottom, bottom-to-top (-1 absent)
   int grp;              // rows per local-GSPN group (H: global)
   int renorm;           // Eq. 6 logits (LG kernels): normalise over on-line neighbours only
+  int y_pd;             // dy is (n, B, C, H, W): the direction's map at slot * npc
 };
 
 // LG: the weight maps hold Eq. 6 logits; dw becomes their gradient.
@@ -469,7 +471,8 @@ __global__ void __launch_bounds__((BOTH ? 128 : 64) * WPD, 2) large_vadj_kernel(
   __syncthreads();
 
   const T* w0 = (const T*)p.w + (int64_t)slot * 3 * p.npc + pb;
-  const T* base[5] = {(const T*)p.dy + pb, (const T*)p.u + pb, w0, w0 + p.npc, w0 + 2 * p.npc};
+  const T* dyb = (const T*)p.dy + (p.y_pd ? (int64_t)slot * p.npc : 0);
+  const T* base[5] = {dyb + pb, (const T*)p.u + pb, w0, w0 + p.npc, w0 + 2 * p.npc};
   T* d0 = (T*)p.dw + (int64_t)slot * 3 * p.npc + pb;
   const float* hb = p.h[dir] + pb;
   float* gs = p.gsum + pb;
@@ -705,6 +708,7 @@ hipError_t large_bwd_v_adj_t(const LargeBwdVAdjArgs& a) {
   p.slot[0] = a.slot_t2b; p.slot[1] = a.slot_b2t;
   p.grp = (a.group > 0 && a.group < a.H) ? a.group : a.H;
   p.renorm = a.renorm;
+  p.y_pd = a.y_pd;
   const bool both = a.slot_t2b >= 0 && a.slot_b2t >= 0, lg = a.logits != 0;
   hipStream_t st = (hipStream_t)a.stream;
   switch (g.wpd) {

@@ -65,6 +65,7 @@ struct LargeVParams {
   int split;
   int grp;           // rows per local-GSPN group (H: the global scan)
   int renorm;        // Eq. 6 logits (LG kernels): normalise over on-line neighbours only
+  int y_pd;          // unmerged outputs: y is (n, B, C, H, W), this direction's map at slot * npc
 };
 
 // Layout of a row over a wave: the wave's span of 64 * NP positions is cut into
@@ -251,7 +252,7 @@ __device__ __forceinline__ void large_v_body(const LargeVParams& p) {
           if constexpr (fin) {
 #pragma unroll
             for (int j = 0; j < G; ++j) o[j] *= uring[ka][q].get(j);
-            stv<G>((T*)p.y + pb + off + po[q], o);
+            stv<G>((T*)p.y + (p.y_pd ? (int64_t)slot * p.npc : 0) + pb + off + po[q], o);
           } else {
             stv<G>(p.acc + pb + off + po[q], o);
           }
@@ -353,6 +354,12 @@ struct LargeHParams {
   int rec;
   float* hbuf;
   int renorm;         // Eq. 6 logits (LG kernels): normalise over on-line neighbours only
+  // unmerged outputs: each direction writes y_d = u * h_d to its own map
+  // (slot * npc); nothing is combined
+  int y_pd;
+  // rec mode with unmerged outputs: acc (+)= dy_d * h instead of h (dy_d: this
+  // direction's output gradient), the sum du needs
+  const void* hdy;
 };
 
 // LG: the weight maps hold Eq. 6 logits, normalised as they are unpacked.
@@ -420,10 +427,12 @@ __device__ __forceinline__ void large_h_body(const LargeHParams& p) {
   // epilogue operands: the first UP vectors of each thread are requested
   // during the last quarter of the scan (their tile registers are dead by
   // then), so the epilogue finds them in registers
-  const bool second = both && p.step >= p.half;
-  const bool fin = !p.rec && (!both || second);
-  const bool read_acc = second || p.has_v;
-  const bool add_b = p.acc_b != nullptr && !second;  // the vertical sum still lives in two arrays
+  const bool second = both && p.step >= p.half && !p.y_pd;
+  const bool fin = !p.rec && (!both || second || p.y_pd);
+  const bool read_acc = (second || p.has_v) && !p.y_pd;
+  const bool add_b = p.acc_b != nullptr && !second && !p.y_pd;  // the vertical sum still lives in two arrays
+  T* const yout = (T*)p.y + (p.y_pd ? (int64_t)slot * p.npc : 0);
+  const T* const hdy = (const T*)p.hdy;
   const int rows = min(p.band_rows, H - band * p.band_rows);
   const int nvr = (K - lo) / VE;
   const int n = rows * nvr;
@@ -440,6 +449,7 @@ __device__ __forceinline__ void large_h_body(const LargeHParams& p) {
       if (read_acc) ldv<VE>(p.acc + o, pav[k]);
       if (add_b) ldv<VE>(p.acc_b + o, pbv[k]);
       if (fin) puv[k].load((const T*)p.u + o);
+      if (hdy) puv[k].load(hdy + o);  // rec mode: the direction's dy (u is not needed there)
     }
   };
 
@@ -512,12 +522,15 @@ __device__ __forceinline__ void large_h_body(const LargeHParams& p) {
     const int64_t o = ob + (int64_t)rr * W + cc;
     float s[VE];
 #pragma unroll
-    for (int q = 0; q < VE; ++q) s[q] = (read_acc ? (add_b ? av[q] + bv[q] : av[q]) : 0.f) + lds[rr * KP + cc + q];
+    for (int q = 0; q < VE; ++q) {
+      const float hv = hdy ? lds[rr * KP + cc + q] * uv.get(q) : lds[rr * KP + cc + q];
+      s[q] = (read_acc ? (add_b ? av[q] + bv[q] : av[q]) : 0.f) + hv;
+    }
     if (p.rec) stv<VE>(p.hbuf + o, lds + rr * KP + cc);
     if (fin) {
 #pragma unroll
       for (int q = 0; q < VE; ++q) s[q] *= uv.get(q);
-      stv<VE>((T*)p.y + o, s);
+      stv<VE>(yout + o, s);
     } else {
       stv<VE>(p.acc + o, s);
     }
@@ -537,6 +550,7 @@ __device__ __forceinline__ void large_h_body(const LargeHParams& p) {
       if (read_acc) ldv<VE>(p.acc + o, av[k]);
       if (add_b) ldv<VE>(p.acc_b + o, bv[k]);
       if (fin) uv[k].load((const T*)p.u + o);
+      if (hdy) uv[k].load(hdy + o);
     }
 #pragma unroll
     for (int k = 0; k < U; ++k)
@@ -665,6 +679,12 @@ hipError_t large_fwd_t(const LargeFwdArgs& a) {
     v.grp = (a.group_h > 0 && a.group_h < a.H) ? a.group_h : a.H;
     v.split = slot[0] >= 0 && slot[1] >= 0 && has_h && a.acc_b != nullptr;
     v.renorm = a.renorm;
+    if (a.y_pd) {
+      // unmerged outputs: every direction writes its own y, nothing is summed
+      v.final_out = 1;
+      v.split = slot[0] >= 0 && slot[1] >= 0;
+      v.y_pd = 1;
+    }
     v.acc_b = a.acc_b;
     if (v.split && 2 * a.planes > 0x7fffffffLL) return hipErrorInvalidConfiguration;
     const bool both = slot[0] >= 0 && slot[1] >= 0 && !v.split;
@@ -687,9 +707,10 @@ hipError_t large_fwd_t(const LargeFwdArgs& a) {
   h.delay = both ? (g.nblk & 1) : 0;
   h.half = both ? g.nblk / 2 + h.delay : 0;
   h.band_rows = g.band_rows; h.nbands = g.nbands; h.halo = g.halo;
-  h.has_v = has_v ? 1 : 0;
+  h.has_v = has_v && !a.y_pd ? 1 : 0;
   h.renorm = a.renorm;
-  h.acc_b = (slot[0] >= 0 && slot[1] >= 0 && a.acc_b != nullptr) ? a.acc_b : nullptr;
+  h.y_pd = a.y_pd;
+  h.acc_b = (slot[0] >= 0 && slot[1] >= 0 && a.acc_b != nullptr && !a.y_pd) ? a.acc_b : nullptr;
   const int64_t grid = (int64_t)g.nbands * a.planes * (both ? 2 : 1);
   if (grid > 0x7fffffffLL) return hipErrorInvalidConfiguration;
   const int GW = (a.group_w > 0 && a.group_w < a.W) ? a.group_w : a.W;

@@ -72,12 +72,15 @@ struct GradFinishArgs {
   const float* hsum;
   const float* hsum2;  // further parts of sum_d h_d (null when absent)
   const float* hsum3;
+  const void* dy2;     // du_mode 3: du = hsum + dy2 * hsum2 + dy3 * hsum3 (unmerged outputs)
+  const void* dy3;
   void* dx;
   void* dlam;         // null when dlam was written per direction
   void* du;
   int64_t n;
   int dx_mode;        // 0: dx = lam * gsum; 1: dx = gsum
-  int du_mode;        // 0: du = dy * hsum; 1: du = hsum; 2: du written per direction
+  int du_mode;        // 0: du = dy * hsum; 1: du = hsum; 2: du written per direction;
+                      // 3: du = hsum + dy2 * hsum2 + dy3 * hsum3
   int dtype;
   void* stream;
 };
@@ -152,6 +155,7 @@ struct LargeFwdArgs {
   int H, W, dtype;
   int group_h, group_w;  // local-GSPN group lengths (0: global)
   int logits, renorm;    // w holds Eq. 6 logits (renorm: over on-line neighbours only)
+  int y_pd;              // unmerged outputs (y is (n, B, C, H, W)); no partial sums needed
   void* stream;
 };
 hipError_t large_fwd_f32(const LargeFwdArgs& a);
@@ -179,6 +183,7 @@ struct LargeBwdHArgs {
   int H, W;
   int group;         // columns per local-GSPN group (0 or >= W: global)
   int logits, renorm;  // w holds Eq. 6 logits; dw is the gradient for the logits
+  const void* hdy;   // unmerged outputs: this direction's dy; hsum (+)= dy * h
   void* stream;
 };
 
@@ -219,6 +224,7 @@ struct LargeBwdVAdjArgs {
   int H, W;
   int group;
   int logits, renorm;  // w holds Eq. 6 logits; dw is the gradient for the logits
+  int y_pd;            // dy is (n, B, C, H, W): each direction's seed from its own map
   void* stream;
 };
 hipError_t large_bwd_v_adj_f32(const LargeBwdVAdjArgs& a);

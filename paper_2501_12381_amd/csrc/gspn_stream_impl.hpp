@@ -434,6 +434,7 @@ __global__ void __launch_bounds__(256)
 grad_finish_kernel(const T* __restrict__ x, const T* __restrict__ lam, const T* __restrict__ dy,
                    const float* __restrict__ gsum, const float* __restrict__ hsum,
                    const float* __restrict__ hsum2, const float* __restrict__ hsum3,
+                   const T* __restrict__ dy2, const T* __restrict__ dy3,
                    T* __restrict__ dx, T* __restrict__ dlam, T* __restrict__ du, int64_t n,
                    int dx_mode, int du_mode) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x * VEC;
@@ -456,6 +457,25 @@ grad_finish_kernel(const T* __restrict__ x, const T* __restrict__ lam, const T* 
     }
     if (du_mode == 2) continue;
     ldv<VEC>(hsum + i, hs);
+    if (du_mode == 3) {
+      // unmerged outputs: hsum already holds dy_d h_d of its directions; the
+      // vertical ones are weighted by their own dy here
+      float b[VEC];
+      if (hsum2) {
+        ldv<VEC>(hsum2 + i, a);
+        ldv<VEC>(dy2 + i, b);
+#pragma unroll
+        for (int q = 0; q < VEC; ++q) hs[q] = fmaf(b[q], a[q], hs[q]);
+      }
+      if (hsum3) {
+        ldv<VEC>(hsum3 + i, a);
+        ldv<VEC>(dy3 + i, b);
+#pragma unroll
+        for (int q = 0; q < VEC; ++q) hs[q] = fmaf(b[q], a[q], hs[q]);
+      }
+      stv<VEC>(du + i, hs);
+      continue;
+    }
     if (hsum2) {
       ldv<VEC>(hsum2 + i, a);
 #pragma unroll
@@ -628,8 +648,8 @@ hipError_t grad_finish_t(const GradFinishArgs& a) {
   const int64_t n = a.n;
   bool vec = n % 8 == 0;
   for (const void* q : {(const void*)a.x, (const void*)a.lam, (const void*)a.dy, (const void*)a.gsum,
-                        (const void*)a.hsum, (const void*)a.hsum2, (const void*)a.hsum3, (const void*)a.dx,
-                        (const void*)a.dlam, (const void*)a.du})
+                        (const void*)a.hsum, (const void*)a.hsum2, (const void*)a.hsum3, a.dy2, a.dy3,
+                        (const void*)a.dx, (const void*)a.dlam, (const void*)a.du})
     if ((uintptr_t)q % 16) vec = false;
   const int per = vec ? 8 : 1;
   int64_t blocks = (n / per + 255) / 256;
@@ -638,7 +658,8 @@ hipError_t grad_finish_t(const GradFinishArgs& a) {
   auto kern = vec ? grad_finish_kernel<T, 8> : grad_finish_kernel<T, 1>;
   hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)a.stream,
                      (const T*)a.x, (const T*)a.lam, (const T*)a.dy, a.gsum, a.hsum, a.hsum2, a.hsum3,
-                     (T*)a.dx, (T*)a.dlam, (T*)a.du, n, a.dx_mode, a.du_mode);
+                     (const T*)a.dy2, (const T*)a.dy3, (T*)a.dx, (T*)a.dlam, (T*)a.du, n, a.dx_mode,
+                     a.du_mode);
   return hipGetLastError();
 }
 

@@ -156,10 +156,11 @@ def test_fwd_rejects_bad_arguments(lib):
     assert fwd(group_w=-2) == 7
     # per-direction maps: the resident forward takes unmerged outputs and
     # per-direction lam, not a merged y with per-direction u; the two-pass
-    # family takes none of them (forcing it is refused)
+    # family takes unmerged outputs only (forcing a family that does not take a
+    # flag is refused)
     assert fwd(algo=L.GSPN_ALGO_RESIDENT, flags=L.GSPN_FLAG_U_PER_DIR) == 7
     assert fwd(algo=L.GSPN_ALGO_RESIDENT_GENERIC, flags=L.GSPN_FLAG_W_LOGITS | L.GSPN_FLAG_U_PER_DIR) == 7
-    assert fwd(algo=L.GSPN_ALGO_TWO_PASS, W=64, dtype=L.GSPN_BF16, flags=L.GSPN_FLAG_Y_PER_DIR) == 7
+    assert fwd(algo=L.GSPN_ALGO_TWO_PASS, W=64, dtype=L.GSPN_BF16, flags=L.GSPN_FLAG_U_PER_DIR | L.GSPN_FLAG_Y_PER_DIR) == 7
     # per-direction maps are n times larger: y (4 maps of 512 bytes) overlaps u's
     # second map, lam's fourth map reaches into y
     assert fwd(flags=L.GSPN_FLAG_U_PER_DIR, y=FAKE + (3 << 30) + 512) == 6

@@ -273,6 +273,21 @@ def test_per_direction_maps_resident(shape, pd, algo):
     check_bwd(inp, mask, algo, torch.bfloat16, f"per-dir {shape} {pd}", **opt)
 
 
+@pytest.mark.parametrize("algo", [0, 4], ids=lambda a: ALGO_NAMES[a])
+@pytest.mark.parametrize("mask", [15, 5, 12, 9])
+@pytest.mark.parametrize("shape", [(64, 128), (128, 128), (600, 136)], ids=lambda s: f"{s[0]}x{s[1]}")
+def test_per_direction_outputs_two_pass(shape, mask, algo):
+    """Unmerged outputs (and dy) on the two-pass family, with logits: every
+    direction writes its own y_d; the backward seeds each direction from its
+    own dy_d and forms du = sum_d dy_d h_d."""
+    H, W = shape
+    print(f"[opt] two-pass unmerged {shape} mask {mask} {ALGO_NAMES[algo]}", flush=True)
+    inp = inputs(1, 2, H, W, mask, torch.bfloat16, seed=H + W + mask, y_pd=True, logits=True)
+    opt = dict(y_per_dir=True, logits=True)
+    check_fwd(inp, mask, algo, torch.bfloat16, f"two-pass unmerged {shape}", **opt)
+    check_bwd(inp, mask, algo, torch.bfloat16, f"two-pass unmerged {shape}", **opt)
+
+
 def test_all_options_together_autograd():
     """Groups, logits with edge renormalisation and per-direction maps through
     the autograd wrapper."""
