@@ -108,6 +108,17 @@ __device__ __forceinline__ float from_next_lane(float v) {
                                                             0xf, 0xf, true));
 }
 
+// the same shifts without the bound control: the lane without a source keeps
+// `edge` (its neighbour from outside the wave), so no select is needed
+__device__ __forceinline__ float from_prev_lane_or(float v, float edge) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, edge),
+                                                               __builtin_bit_cast(int, v), 0x138, 0xf, 0xf, false));
+}
+__device__ __forceinline__ float from_next_lane_or(float v, float edge) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, edge),
+                                                               __builtin_bit_cast(int, v), 0x130, 0xf, 0xf, false));
+}
+
 // Workgroup barrier that orders LDS accesses only: waits for this wave's LDS
 // operations, then for every wave.  Global loads stay in flight across it
 // (a full __syncthreads would drain them), which keeps register prefetches

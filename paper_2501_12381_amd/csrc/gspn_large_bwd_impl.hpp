@@ -7,8 +7,9 @@
 //   recompute  large_hrec_kernel (pass H in its `rec` mode), blocks in scan order: h of
 //              the direction into an fp32 plane `hbuf`, and hsum (+)= h.
 //   adjoint    large_hadj_kernel, blocks in reverse scan order.  A workgroup
-//              owns a band of rows plus a halo of K rows on each side (one
-//              row per lane), as in the forward: starting from the exact
+//              owns a band of rows plus a halo of K rows towards each
+//              neighbouring band (one row per lane), as in the forward:
+//              starting from the exact
 //              products of the column after the block (carried between
 //              launches in a small workspace), the transposed stencil
 //                g[l][p] = u dy[l][p] + w0[n][p+1] g[n][p+1] + w1[n][p] g[n][p]
@@ -49,7 +50,7 @@ struct LargeHAdjParams {
   int H, W;
   int first;           // store gsum instead of adding
   int step, nblk;
-  int band_rows, nbands, halo;
+  int band_rows, edge_rows, nbands, halo;  // bands as in the forward's pass H
   // bit i: window column i takes nothing from the next line (that line starts
   // a group); bit i of gmask: window column i starts a group (zero previous state)
   uint64_t zmask, gmask;
@@ -68,8 +69,11 @@ __global__ void __launch_bounds__(64 * NW) large_hadj_kernel(LargeHAdjParams p) 
   constexpr int HOFF = DIR ? 0 : 4;   // LDS column of window column 0
   constexpr int PREV = DIR ? 1 : -1;  // window offset of the scan-previous column
   typedef Pack<T, VE> PK;
-  extern __shared__ float lds[];      // [band_rows + 2][HP]; edges [2][NW][2]; 64 dummy slots
-  float* edge = lds + (p.band_rows + 2) * HP;
+  // [edge_rows + 2][HP]; edges [2 parities][NW + 2][2] (wave w at slot w + 1,
+  // zeros at slots 0 and NW + 1); 64 dummy slots
+  extern __shared__ float lds[];
+  float* edge = lds + (p.edge_rows + 2) * HP;
+  constexpr int ES = (NW + 2) * 2;
 
   // workgroup -> (plane, band); the bands of a plane share an XCD
   const int64_t G = gridDim.x, b = blockIdx.x;
@@ -84,13 +88,18 @@ __global__ void __launch_bounds__(64 * NW) large_hadj_kernel(LargeHAdjParams p) 
   const int lo = c0 - ws;  // first window column of this block
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int used = p.band_rows + 2 * p.halo;
-  const int r = band * p.band_rows - p.halo + (tid < used ? tid : used - 1);
+  // kept rows [bs, be); halo rows only towards a neighbouring band
+  const bool last = band == p.nbands - 1;
+  const int bs = band == 0 ? 0 : p.edge_rows + (band - 1) * p.band_rows;
+  const int be = last ? H : min(H, bs + (band == 0 ? p.edge_rows : p.band_rows));
+  const int htop = band == 0 ? 0 : p.halo;
+  const int used = be - bs + htop + (last ? 0 : p.halo);
+  const int r = bs - htop + (tid < used ? tid : used - 1);
   const bool row_ok = tid < used && r >= 0 && r < H;
   const int rc = r < 0 ? 0 : (r >= H ? H - 1 : r);
-  const int br = tid - p.halo;
-  const bool in_band = br >= 0 && br < p.band_rows && row_ok;
-  const int rows = min(p.band_rows, H - band * p.band_rows);  // band rows inside the plane
+  const int br = r - bs;
+  const bool in_band = row_ok && br >= 0 && br < be - bs;
+  const int rows = be - bs;
 
   const int64_t HW = (int64_t)H * W;
   const int64_t rb = plane * HW + (int64_t)rc * W + ws;
@@ -110,9 +119,9 @@ __global__ void __launch_bounds__(64 * NW) large_hadj_kernel(LargeHAdjParams p) 
   // HOFF, into LDS (zero outside the plane)
   {
     constexpr int NV = HC / 4;  // float4 vectors per LDS row
-    const int nrow = p.band_rows + 2;
+    const int nrow = rows + 2;
     const int nvec = nrow * NV;
-    const int r0 = band * p.band_rows - 1;
+    const int r0 = bs - 1;
     const int cb = ws - HOFF;
     const float* hp0 = p.hbuf + plane * HW;
     constexpr int TT = 64 * NW, UB = 4;
@@ -150,10 +159,11 @@ __global__ void __launch_bounds__(64 * NW) large_hadj_kernel(LargeHAdjParams p) 
   }
   if (!row_ok) a0 = a1 = a2 = 0.f;
   // wave edges: lane 0 publishes its a0 (row above it reads it), lane 63 its a2
-  if (lane == 0) edge[(1 * NW + wave) * 2 + 0] = a0;
-  if (lane == 63) edge[(1 * NW + wave) * 2 + 1] = a2;
+  if (lane == 0) edge[ES + (wave + 1) * 2 + 0] = a0;
+  if (lane == 63) edge[ES + (wave + 1) * 2 + 1] = a2;
+  if (tid < 8) edge[((tid >> 2) & 1) * ES + ((tid >> 1) & 1) * ((NW + 1) * 2) + (tid & 1)] = 0.f;  // zero slots
   auto eslot = [&](int par) {
-    return lane == 0 ? (par * NW + wave) * 2 : (lane == 63 ? (par * NW + wave) * 2 + 1 : 4 * NW + lane);
+    return lane == 0 ? par * ES + (wave + 1) * 2 : (lane == 63 ? par * ES + (wave + 1) * 2 + 1 : 2 * ES + lane);
   };
   const int eo0 = eslot(0), eo1 = eslot(1);
   float* hrow = lds + (in_band ? br + 1 : 1) * HP;  // this row's h (then g) in LDS
@@ -171,13 +181,13 @@ __global__ void __launch_bounds__(64 * NW) large_hadj_kernel(LargeHAdjParams p) 
     if (ti < lo) return;                     // columns of the next block (uniform)
     const int par = i & 1;
     const bool zr = (zm >> ti) & 1;
-    float an = from_next_lane(a0), ap = from_prev_lane(a2);
+    // products from the adjacent waves (zero slots past the first and last)
+    float nd = 0.f, nu = 0.f;
     if constexpr (NW > 1) {
-      const float nd = edge[((par ^ 1) * NW + (wave < NW - 1 ? wave + 1 : wave)) * 2 + 0];
-      const float nu = edge[((par ^ 1) * NW + (wave > 0 ? wave - 1 : wave)) * 2 + 1];
-      if (lane == 63) an = wave < NW - 1 ? nd : 0.f;
-      if (lane == 0) ap = wave > 0 ? nu : 0.f;
+      nd = edge[(par ^ 1) * ES + (wave + 2) * 2 + 0];
+      nu = edge[(par ^ 1) * ES + wave * 2 + 1];
     }
+    const float an = from_next_lane_or(a0, nd), ap = from_prev_lane_or(a2, nu);
     float gin = a1 + an + ap;
     gin = zr ? 0.f : gin;
     const float dyv = tile[0][ti / VE].get(ti % VE), uv = tile[1][ti / VE].get(ti % VE);
@@ -247,7 +257,7 @@ __global__ void __launch_bounds__(64 * NW) large_hadj_kernel(LargeHAdjParams p) 
   // gsum (+)= g over the band rows and the block's columns, 4 floats a thread
   const int nvr = (K - lo) / 4;
   const int n = rows * nvr;
-  const int64_t ob = plane * HW + (int64_t)band * p.band_rows * W + ws;
+  const int64_t ob = plane * HW + (int64_t)bs * W + ws;
   constexpr int TT = 64 * NW, U = 8;
   for (int e0 = tid; e0 < n; e0 += TT * U) {
     float av[U][4];
@@ -313,7 +323,7 @@ hipError_t large_bwd_h_t(const LargeBwdHArgs& a) {
   const LargeGeom<T> g = large_geom<T>(a.H, a.W);
   hipStream_t st = (hipStream_t)a.stream;
   const int64_t npc = a.planes * (int64_t)a.H * a.W;
-  const int64_t grid = (int64_t)g.nbands * a.planes;
+  const int64_t grid = (int64_t)g.hb_n * a.planes;
   if (grid > 0x7fffffffLL) return hipErrorInvalidConfiguration;
   const int GW = (a.group > 0 && a.group < a.W) ? a.group : a.W;
   // scan order: left-to-right visits column c after c - 1, right-to-left after c + 1
@@ -331,7 +341,7 @@ hipError_t large_bwd_h_t(const LargeBwdHArgs& a) {
   h.slot0 = a.dir ? -1 : 0;
   h.slot1 = a.dir ? 0 : -1;
   h.nblk = g.nblk; h.delay = 0; h.half = 0;
-  h.band_rows = g.band_rows; h.nbands = g.nbands; h.halo = g.halo;
+  h.band_rows = g.hb_mid; h.edge_rows = g.hb_edge; h.nbands = g.hb_n; h.halo = g.halo;
   h.has_v = a.first ? 0 : 1;
   h.acc_b = nullptr;
   h.rec = 1;
@@ -348,7 +358,7 @@ hipError_t large_bwd_h_t(const LargeBwdHArgs& a) {
     h.step = j;
     h.gmask[0] = a.dir ? 0 : m;
     h.gmask[1] = a.dir ? m : 0;
-    hipError_t e = launch_large_h<T>(h, g.nw, grid, g.lds_h, a.logits != 0, st);
+    hipError_t e = launch_large_h<T>(h, g.hb_nw, grid, g.lds_hb, a.logits != 0, st);
     if (e != hipSuccess) return e;
   }
 
@@ -359,8 +369,8 @@ hipError_t large_bwd_h_t(const LargeBwdHArgs& a) {
   p.first = a.first;
   p.renorm = a.renorm;
   p.nblk = g.nblk;
-  p.band_rows = g.band_rows; p.nbands = g.nbands; p.halo = g.halo;
-  const size_t lds = ((size_t)(g.band_rows + 2) * (K + 5) + 4 * 8 + 64) * sizeof(float);
+  p.band_rows = g.hb_mid; p.edge_rows = g.hb_edge; p.nbands = g.hb_n; p.halo = g.halo;
+  const size_t lds = ((size_t)(g.hb_edge + 2) * (K + 5) + 4 * (8 + 2) + 64) * sizeof(float);
   for (int j = 0; j < g.nblk; ++j) {
     const int blk = a.dir ? j : g.nblk - 1 - j;
     const int ws = window(blk);
@@ -374,7 +384,7 @@ hipError_t large_bwd_h_t(const LargeBwdHArgs& a) {
     p.step = j;
     p.zmask = zm;
     p.gmask = gm;
-    hipError_t e = launch_large_hadj<T>(p, a.dir, g.nw, grid, lds, a.logits != 0, st);
+    hipError_t e = launch_large_hadj<T>(p, a.dir, g.hb_nw, grid, lds, a.logits != 0, st);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;

@@ -12,7 +12,9 @@
 //           the middle row it adds its h to what the other direction stored.
 //   pass H  (one launch per block of K columns, K = 128 bytes of a row):
 //           left-to-right and right-to-left.  A workgroup owns a band of rows
-//           plus a halo of K rows on each side, one row per lane, and holds the
+//           plus a halo of K rows on each side that has a neighbouring band
+//           (the first and last bands keep K more rows instead), one row per
+//           lane, and holds the
 //           block's K columns of each input as 128-byte row segments in
 //           registers, so every cache line of a row is read by one load.
 //           Starting from the exact state of the previous block (a column of
@@ -343,7 +345,9 @@ struct LargeHParams {
   int nblk;           // column blocks
   int delay;          // right-to-left starts one launch late (odd block count, both present)
   int half;           // first launch of the second half (pairs)
-  int band_rows, nbands, halo;
+  // bands: the first and last keep edge_rows rows (one halo each), the others
+  // band_rows (halo rows above and below); one band keeps the whole plane
+  int band_rows, edge_rows, nbands, halo;
   int has_v;          // acc holds the vertical pass's partial sum
   const float* acc_b; // non-null: the vertical sum is acc + acc_b until the first horizontal direction adds
   // local GSPN, per direction (left-to-right, right-to-left): bit i set when
@@ -368,8 +372,12 @@ __device__ __forceinline__ void large_h_body(const LargeHParams& p) {
   using C = LargeCfg<T>;
   constexpr int K = C::KH, HV = C::HV, VE = C::VE, KP = K + 1;
   typedef Pack<T, VE> PK;
-  extern __shared__ float lds[];  // [band_rows][KP] h of the band, edges [2][NW][2], 64 dummy slots
-  float* edge = lds + p.band_rows * KP;
+  // [edge_rows][KP] h of the band; edges [2 parities][NW + 2][2]: wave w's first
+  // and last rows at slot w + 1, zeros at slots 0 and NW + 1 (no neighbour
+  // wave); 64 dummy slots
+  extern __shared__ float lds[];
+  float* edge = lds + p.edge_rows * KP;
+  constexpr int ES = (NW + 2) * 2;  // floats per parity
 
   // workgroup -> (direction, plane, band); consecutive ids (the bands of a plane,
   // which share halo rows) are placed on the same XCD
@@ -393,13 +401,19 @@ __device__ __forceinline__ void large_h_body(const LargeHParams& p) {
   const int lo = c0 - ws;  // first valid column of the window
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // kept rows [bs, be) of the band; halo rows only towards a neighbouring band,
+  // so every lane in use holds a row of the plane
+  const bool last = band == p.nbands - 1;
+  const int bs = band == 0 ? 0 : p.edge_rows + (band - 1) * p.band_rows;
+  const int be = last ? H : min(H, bs + (band == 0 ? p.edge_rows : p.band_rows));
+  const int htop = band == 0 ? 0 : p.halo;
+  const int used = be - bs + htop + (last ? 0 : p.halo);
   // lanes past the band and its halos duplicate the last row in use (no traffic)
-  const int used = p.band_rows + 2 * p.halo;
-  const int r = band * p.band_rows - p.halo + (tid < used ? tid : used - 1);
+  const int r = bs - htop + (tid < used ? tid : used - 1);
   const bool row_ok = tid < used && r >= 0 && r < H;
   const int rc = r < 0 ? 0 : (r >= H ? H - 1 : r);
-  const int br = tid - p.halo;  // row inside the band
-  const bool in_band = br >= 0 && br < p.band_rows && row_ok;
+  const int br = r - bs;  // row inside the band
+  const bool in_band = row_ok && br >= 0 && br < be - bs;
 
   const int64_t HW = (int64_t)H * W;
   const int64_t rb = plane * HW + (int64_t)rc * W + ws;
@@ -414,14 +428,16 @@ __device__ __forceinline__ void large_h_body(const LargeHParams& p) {
     hp = sin[rc];
   }
   hp = row_ok ? hp : 0.f;
-  if (lane == 0) edge[(1 * NW + wave) * 2 + 0] = hp;
-  if (lane == 63) edge[(1 * NW + wave) * 2 + 1] = hp;
+  if (lane == 0) edge[ES + (wave + 1) * 2 + 0] = hp;
+  if (lane == 63) edge[ES + (wave + 1) * 2 + 1] = hp;
+  if (tid < 4) edge[(tid >> 1) * ES + (tid & 1) * ((NW + 1) * 2)] = 0.f;  // slots 0 and NW + 1, first row
+  if (tid >= 4 && tid < 8) edge[((tid - 4) >> 1) * ES + ((tid - 4) & 1) * ((NW + 1) * 2) + 1] = 0.f;  // ... last row
 
   float* hrow = lds + (in_band ? br : 0) * KP;
   // edge slot of this lane per step parity: lanes 0 and 63 publish their row's
   // h for the neighbouring waves, the other lanes write a private dummy slot
   auto eslot = [&](int par) {
-    return lane == 0 ? (par * NW + wave) * 2 : (lane == 63 ? (par * NW + wave) * 2 + 1 : 4 * NW + lane);
+    return lane == 0 ? par * ES + (wave + 1) * 2 : (lane == 63 ? par * ES + (wave + 1) * 2 + 1 : 2 * ES + lane);
   };
   const int eo0 = eslot(0), eo1 = eslot(1);
   // epilogue operands: the first UP vectors of each thread are requested
@@ -433,10 +449,10 @@ __device__ __forceinline__ void large_h_body(const LargeHParams& p) {
   const bool add_b = p.acc_b != nullptr && !second && !p.y_pd;  // the vertical sum still lives in two arrays
   T* const yout = (T*)p.y + (p.y_pd ? (int64_t)slot * p.npc : 0);
   const T* const hdy = (const T*)p.hdy;
-  const int rows = min(p.band_rows, H - band * p.band_rows);
+  const int rows = be - bs;
   const int nvr = (K - lo) / VE;
   const int n = rows * nvr;
-  const int64_t ob = plane * HW + (int64_t)band * p.band_rows * W + ws;
+  const int64_t ob = plane * HW + (int64_t)bs * W + ws;
   constexpr int TT = 64 * NW, UP = 6, PF = K - K / 4;
   float pav[UP][VE], pbv[UP][VE];
   Pack<T, VE> puv[UP];
@@ -477,15 +493,18 @@ __device__ __forceinline__ void large_h_body(const LargeHParams& p) {
       const int ti = REV ? K - 1 - i : i;  // window column of this step
       if (ti < lo) return;                 // short last block (uniform)
       const int par = i & 1;
-      const bool rst = (gm >> ti) & 1;  // this column starts a group (uniform)
-      if (rst) hp = 0.f;
-      float up = from_prev_lane(hp), dn = from_next_lane(hp);
+      // neighbours from the adjacent waves (zero slots past the first and last)
+      float nu = 0.f, nd = 0.f;
       if constexpr (NW > 1) {
-        const float nu = edge[((par ^ 1) * NW + (wave > 0 ? wave - 1 : wave)) * 2 + 1];
-        const float nd = edge[((par ^ 1) * NW + (wave < NW - 1 ? wave + 1 : wave)) * 2 + 0];
-        if (lane == 0) up = (wave > 0 && !rst) ? nu : 0.f;
-        if (lane == 63) dn = (wave < NW - 1 && !rst) ? nd : 0.f;
+        nu = edge[(par ^ 1) * ES + wave * 2 + 1];
+        nd = edge[(par ^ 1) * ES + (wave + 2) * 2 + 0];
       }
+      if ((gm >> ti) & 1) {  // this column starts a group: the state restarts (uniform)
+        hp = 0.f;
+        nu = 0.f;
+        nd = 0.f;
+      }
+      const float up = from_prev_lane_or(hp, nu), dn = from_next_lane_or(hp, nd);
       const float xv = tile[0][ti / VE].get(ti % VE), lv = tile[1][ti / VE].get(ti % VE);
       float a = tile[2][ti / VE].get(ti % VE), bw = tile[3][ti / VE].get(ti % VE),
             cw = tile[4][ti / VE].get(ti % VE);
@@ -581,9 +600,11 @@ inline bool large_fwd_supported(int H, int W) {
 template <typename T>
 struct LargeGeom {
   int wpd;        // vertical: waves per direction (power of two)
-  int band_rows, nbands, halo, nw;
+  // horizontal bands (forward, recompute and adjoint): the first and last keep
+  // hb_edge rows (one halo of `halo` rows), the others hb_mid (two halos)
+  int hb_n, hb_mid, hb_edge, hb_nw, halo;
   int nblk;
-  size_t lds_h;   // dynamic LDS of pass H
+  size_t lds_hb;  // dynamic LDS of pass H
 };
 
 template <typename T>
@@ -594,19 +615,19 @@ inline LargeGeom<T> large_geom(int H, int W) {
   g.wpd = 1;
   while (g.wpd < need) g.wpd *= 2;
   if (H <= C::HROWS) {
-    g.nbands = 1;
-    g.band_rows = H;
+    g.hb_n = 1;
+    g.hb_mid = g.hb_edge = H;
     g.halo = 0;
-    g.nw = (H + 63) / 64;
   } else {
-    const int core = C::HROWS - 2 * C::KH;
-    g.nbands = (H + core - 1) / core;
-    g.band_rows = (H + g.nbands - 1) / g.nbands;
+    // every band takes HROWS lanes, the kept rows balanced over the bands
+    g.hb_n = (H - 2 * C::KH + C::HROWS - 2 * C::KH - 1) / (C::HROWS - 2 * C::KH);
+    g.hb_mid = (H - 2 * C::KH + g.hb_n - 1) / g.hb_n;
+    g.hb_edge = g.hb_mid + C::KH;
     g.halo = C::KH;
-    g.nw = (g.band_rows + 2 * C::KH + 63) / 64;
   }
+  g.hb_nw = ((g.hb_n == 1 ? H : g.hb_mid + 2 * C::KH) + 63) / 64;  // lanes: kept rows and halos
   g.nblk = (W + C::KH - 1) / C::KH;
-  g.lds_h = ((size_t)g.band_rows * (C::KH + 1) + 4 * 8 + 64) * sizeof(float);  // h, edges, dummy edge slots
+  g.lds_hb = ((size_t)g.hb_edge * (C::KH + 1) + 4 * (8 + 2) + 64) * sizeof(float);  // h, edges, dummy slots
   return g;
 }
 
@@ -706,12 +727,12 @@ hipError_t large_fwd_t(const LargeFwdArgs& a) {
   h.nblk = g.nblk;
   h.delay = both ? (g.nblk & 1) : 0;
   h.half = both ? g.nblk / 2 + h.delay : 0;
-  h.band_rows = g.band_rows; h.nbands = g.nbands; h.halo = g.halo;
+  h.band_rows = g.hb_mid; h.edge_rows = g.hb_edge; h.nbands = g.hb_n; h.halo = g.halo;
   h.has_v = has_v && !a.y_pd ? 1 : 0;
   h.renorm = a.renorm;
   h.y_pd = a.y_pd;
   h.acc_b = (slot[0] >= 0 && slot[1] >= 0 && a.acc_b != nullptr && !a.y_pd) ? a.acc_b : nullptr;
-  const int64_t grid = (int64_t)g.nbands * a.planes * (both ? 2 : 1);
+  const int64_t grid = (int64_t)g.hb_n * a.planes * (both ? 2 : 1);
   if (grid > 0x7fffffffLL) return hipErrorInvalidConfiguration;
   const int GW = (a.group_w > 0 && a.group_w < a.W) ? a.group_w : a.W;
   // bit i of the mask: window column i of the launch starts a group
@@ -732,7 +753,7 @@ hipError_t large_fwd_t(const LargeFwdArgs& a) {
     h.step = j;
     h.gmask[0] = window_mask(0, j);
     h.gmask[1] = window_mask(1, j - h.delay);
-    hipError_t e = launch_large_h<T>(h, g.nw, grid, g.lds_h, a.logits != 0, st);
+    hipError_t e = launch_large_h<T>(h, g.hb_nw, grid, g.lds_hb, a.logits != 0, st);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
