@@ -441,8 +441,9 @@ __device__ __forceinline__ void large_h_body(const LargeHParams& p) {
   };
   const int eo0 = eslot(0), eo1 = eslot(1);
   // epilogue operands: the first UP vectors of each thread are requested
-  // during the last quarter of the scan (their tile registers are dead by
-  // then), so the epilogue finds them in registers
+  // during the scan, one each time a tile vector of every map has been used
+  // up (the registers it frees hold them), so the epilogue finds them in
+  // registers and the workgroup keeps loads in flight while it scans
   const bool second = both && p.step >= p.half && !p.y_pd;
   const bool fin = !p.rec && (!both || second || p.y_pd);
   const bool read_acc = (second || p.has_v) && !p.y_pd;
@@ -453,20 +454,17 @@ __device__ __forceinline__ void large_h_body(const LargeHParams& p) {
   const int nvr = (K - lo) / VE;
   const int n = rows * nvr;
   const int64_t ob = plane * HW + (int64_t)bs * W + ws;
-  constexpr int TT = 64 * NW, UP = 6, PF = K - K / 4;
+  constexpr int TT = 64 * NW, UP = HV - 1;
   float pav[UP][VE], pbv[UP][VE];
   Pack<T, VE> puv[UP];
-  auto prefetch = [&]() __attribute__((always_inline)) {
-#pragma unroll
-    for (int k = 0; k < UP; ++k) {
-      const int e = tid + k * TT < n ? tid + k * TT : 0;
-      const int rr = e / nvr, cc = lo + (e - rr * nvr) * VE;
-      const int64_t o = ob + (int64_t)rr * W + cc;
-      if (read_acc) ldv<VE>(p.acc + o, pav[k]);
-      if (add_b) ldv<VE>(p.acc_b + o, pbv[k]);
-      if (fin) puv[k].load((const T*)p.u + o);
-      if (hdy) puv[k].load(hdy + o);  // rec mode: the direction's dy (u is not needed there)
-    }
+  auto prefetch = [&](int k) __attribute__((always_inline)) {
+    const int e = tid + k * TT < n ? tid + k * TT : 0;
+    const int rr = e / nvr, cc = lo + (e - rr * nvr) * VE;
+    const int64_t o = ob + (int64_t)rr * W + cc;
+    if (read_acc) ldv<VE>(p.acc + o, pav[k]);
+    if (add_b) ldv<VE>(p.acc_b + o, pbv[k]);
+    if (fin) puv[k].load((const T*)p.u + o);
+    if (hdy) puv[k].load(hdy + o);  // rec mode: the direction's dy (u is not needed there)
   };
 
   const uint64_t gm = p.gmask[dir];
@@ -523,10 +521,12 @@ __device__ __forceinline__ void large_h_body(const LargeHParams& p) {
       if (in_band) hrow[ti] = hp;
       lds_barrier();
     };
-    // two unrolled runs of steps, the epilogue's loads requested between them
-    static_for<0, PF + 1>([&](auto ic) __attribute__((always_inline)) { step(ic); });
-    prefetch();
-    static_for<PF + 1, K>([&](auto ic) __attribute__((always_inline)) { step(ic); });
+    // the steps unrolled; after every VE of them the epilogue's next vector
+    static_for<0, K>([&](auto ic) __attribute__((always_inline)) {
+      step(ic);
+      constexpr int i = decltype(ic)::value;
+      if constexpr ((i + 1) % VE == 0 && (i + 1) / VE - 1 < UP) prefetch((i + 1) / VE - 1);
+    });
   };
   if (dir) scan(std::true_type{});
   else scan(std::false_type{});
