@@ -35,8 +35,17 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found (ROCm is required to build libgspn.so)")
 
 
+# units that take minutes to compile (one large kernel each, or many
+# instantiations); they start first so the parallel build is not left waiting
+# on one of them at the end
+SLOW_UNITS = ("gspn_widebwdlg_", "gspn_large_", "gspn_widebwd_", "gspn_resfwd_", "gspn_hadja_", "gspn_hadjb_",
+              "gspn_widefwd_", "gspn_staged_")
+
+
 def sources() -> list[str]:
-    return sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".hip"))
+    names = sorted(f for f in os.listdir(CSRC) if f.endswith(".hip"))
+    rank = lambda f: next((i for i, p in enumerate(SLOW_UNITS) if f.startswith(p)), len(SLOW_UNITS))
+    return [os.path.join(CSRC, f) for f in sorted(names, key=rank)]
 
 
 def _run(cmd: list[str]) -> None:
