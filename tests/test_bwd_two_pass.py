@@ -2,11 +2,12 @@
 
 The horizontal directions run on the column-block kernels (a recompute of h,
 then the adjoint over blocks in reverse scan order, each workgroup owning a
-band of rows with K halo rows on each side); the vertical ones on the
-streaming kernels.  Cases: one band and several (halo rows crossing band and
+band of rows with K halo rows towards each neighbouring band); the vertical
+ones on the vertical recompute and the paired vertical adjoint.  Cases: one band and several (halo rows crossing band and
 plane edges), ragged last column blocks, every direction set with a
 horizontal direction, several planes, local GSPN groups whose boundaries fall
-inside a column block, and sampled planes of the full 2048 x 2048 workload."""
+inside a column block, row counts around the band-count transitions, and
+sampled planes of the full 2048 x 2048 workload."""
 import numpy as np
 import pytest
 import torch
@@ -15,7 +16,7 @@ import oracle as O
 from paper_2501_12381_amd import lib as L
 from paper_2501_12381_amd import ops, synth
 from paper_2501_12381_amd.synth import WORKLOADS
-from tests.parity_util import assert_close, np64, oracle_bwd
+from tests.parity_util import assert_close, np64, oracle_bwd, oracle_fwd
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
@@ -87,6 +88,24 @@ def test_two_pass_bwd_groups(case, dtype):
     print(f"[bwd2] groups {case} {dtype}", flush=True)
     inp = inputs(1, 2, H, W, 0xF, dtype, seed=H + W * 3 + gh + gw)
     check(inp, 0xF, dtype, f"groups {case}", group_h=gh, group_w=gw)
+
+
+# Row counts around the band-count transitions of the horizontal kernels
+# (every band takes 512 lanes; the first and last keep K more rows than the
+# others, K = 64 columns for bf16 and 32 for fp32): bf16 changes from two to
+# three bands between 896 and 897 rows, fp32 between 960 and 961.
+BAND_EDGE_H = [896, 897, 960, 961, 1281]
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16], ids=["f32", "bf16"])
+@pytest.mark.parametrize("H", BAND_EDGE_H)
+def test_two_pass_band_transitions(H, dtype):
+    print(f"[bwd2] band transition {H} rows {dtype}", flush=True)
+    inp = inputs(1, 1, H, 64, 0xF, dtype, seed=H + 17)
+    y = ops.gspn_scan_fwd(inp["x"], inp["w"], inp["lam"], inp["u"], 0xF, algo=TWO_PASS)
+    torch.cuda.synchronize()
+    assert_close(y, oracle_fwd(inp, 0xF), dtype, f"forward, {H} rows")
+    check(inp, 0xF, dtype, f"backward, {H} rows")
 
 
 def test_two_pass_bwd_deterministic():
