@@ -84,8 +84,25 @@ enum {
   GSPN_FLAG_EDGE_RENORM = 2u, /* with W_LOGITS: normalise over the on-line neighbours only */
   GSPN_FLAG_LAM_PER_DIR = 4u, /* lam and dlam are (n, B, C, H, W) */
   GSPN_FLAG_U_PER_DIR = 8u,   /* u and du are (n, B, C, H, W) */
-  GSPN_FLAG_Y_PER_DIR = 16u   /* y and dy are (n, B, C, H, W): y_d = u_d * h_d, not merged */
+  GSPN_FLAG_Y_PER_DIR = 16u,  /* y and dy are (n, B, C, H, W): y_d = u_d * h_d, not merged */
+  GSPN_FLAG_SAVE_STATE = 32u  /* keep the forward's states for the backward (Alg. 2 takes the
+                                 forward's H as an input): see below */
 };
+
+/* GSPN_FLAG_SAVE_STATE.  Forward: the call also leaves every direction's h and
+ * sum_d h_d (fp32) at the start of its workspace.  Backward (same inputs,
+ * shape, mask, groups, flags and algo): the call reads them there instead of
+ * recomputing the forward scan.  The backward's workspace must therefore begin
+ * with the bytes the forward left: size one buffer with
+ * gspn_scan_bwd_workspace_bytes(..., flags) (which covers the forward's size)
+ * and pass it to both calls, without touching the inputs in between.  dx, dw
+ * and dlam are the same bits as without the flag; du adds the directions in
+ * the forward's order.  Taken by the two-pass family with merged outputs and
+ * a horizontal direction in the mask (the families that keep a plane on chip
+ * recompute there at no HBM cost): the forward then returns GSPN_ERR_ALIGN for
+ * tensors that are not 16-byte aligned instead of falling back to streaming.
+ * For every other problem the flag changes nothing.  gspn_scan_fwd_noalloc
+ * refuses it. */
 
 enum {
   GSPN_DIR_T2B = 1u, /* top to bottom */
@@ -198,7 +215,9 @@ size_t gspn_scan_bwd_workspace_bytes(int64_t B, int64_t C, int64_t H, int64_t W,
  *   outputs dx, dlam, du and dw (shaped like x, lam, u and w), fully
  *   overwritten (not accumulated).  With GSPN_FLAG_W_LOGITS dw is the
  *   gradient with respect to the logits.  The forward state is recomputed
- *   inside, so no tensor from the forward call is needed.
+ *   inside, so no tensor from the forward call is needed (with
+ *   GSPN_FLAG_SAVE_STATE the two-pass family reads the state the forward
+ *   left at the start of the workspace instead).
  */
 int gspn_scan_bwd(const void* dy, const void* x, const void* w, const void* lam, const void* u,
                   void* dx, void* dw, void* dlam, void* du,

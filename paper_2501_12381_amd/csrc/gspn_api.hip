@@ -67,7 +67,7 @@ bool mul_ok(int64_t a, int64_t b, int64_t* out) {
 }
 
 constexpr uint32_t kAllFlags = GSPN_FLAG_W_LOGITS | GSPN_FLAG_EDGE_RENORM | GSPN_FLAG_LAM_PER_DIR |
-                               GSPN_FLAG_U_PER_DIR | GSPN_FLAG_Y_PER_DIR;
+                               GSPN_FLAG_U_PER_DIR | GSPN_FLAG_Y_PER_DIR | GSPN_FLAG_SAVE_STATE;
 
 struct Problem {
   int64_t B, C, H, W, planes, npc;  // npc = elements per (B,C,H,W) tensor
@@ -169,7 +169,8 @@ bool resident_fits(const Problem& p, int dtype, bool backward) {
 // the two-pass family takes unmerged outputs (per-direction y and dy) but not
 // per-direction lam or u
 bool two_pass_fits(const Problem& p, int dtype, bool backward) {
-  if ((p.flags & ~(kEq6Flags | GSPN_FLAG_Y_PER_DIR)) || (p.grouped() && !kTwoPassGroups)) return false;
+  if ((p.flags & ~(kEq6Flags | GSPN_FLAG_Y_PER_DIR | GSPN_FLAG_SAVE_STATE)) || (p.grouped() && !kTwoPassGroups))
+    return false;
   // the backward runs its horizontal directions on the two-pass kernels
   // (their vertical ones on the streaming kernels)
   if (backward && !(p.mask & (DIR_L2R | DIR_R2L))) return false;
@@ -200,7 +201,43 @@ size_t two_pass_state_bytes(const Problem& p, uint32_t mask) {
   return (mask & (DIR_L2R | DIR_R2L)) ? round_up((size_t)4 * p.planes * p.H * 4, kWsAlign) : 0;
 }
 
+// GSPN_FLAG_SAVE_STATE: kept by the two-pass forward (merged outputs, a
+// horizontal direction) as fp32 B*C*H*W arrays at the start of the workspace:
+// the vertical directions' h (top-to-bottom, bottom-to-top), sum_d h_d (the
+// horizontal pass's partial, then final sum), the horizontal directions' h
+// (left-to-right, right-to-left), then the forward's column state.  The
+// backward's own arrays follow.  `fwd_algo` is the family the forward runs.
+constexpr size_t kAbsent = SIZE_MAX;
+bool saves_state(const Problem& p, int fwd_algo) {
+  return fwd_algo == GSPN_ALGO_TWO_PASS && (p.flags & GSPN_FLAG_SAVE_STATE) && !(p.flags & kPdFlags) &&
+         (p.mask & (DIR_L2R | DIR_R2L));
+}
+struct SavedLayout {
+  size_t h[4];  // T2B, B2T, L2R, R2L (kAbsent when the direction is not in the mask)
+  size_t sum, state, total;
+};
+SavedLayout saved_layout(const Problem& p) {
+  const size_t fb = round_up((size_t)p.npc * 4, kWsAlign);
+  SavedLayout l{};
+  size_t off = 0;
+  const int bit[4] = {DIR_T2B, DIR_B2T, DIR_L2R, DIR_R2L};
+  for (int d = 0; d < 2; ++d) l.h[d] = (p.mask & bit[d]) ? (off += fb) - fb : kAbsent;
+  l.sum = off;
+  off += fb;
+  for (int d = 2; d < 4; ++d) l.h[d] = (p.mask & bit[d]) ? (off += fb) - fb : kAbsent;
+  l.state = off;
+  l.total = off + two_pass_state_bytes(p, p.mask);
+  return l;
+}
+// backward reading the kept state: the forward's bytes, the sum of g, the
+// adjoint's column products
+size_t saved_bwd_ws_bytes(const Problem& p) {
+  return saved_layout(p).total + round_up((size_t)p.npc * 4, kWsAlign) +
+         round_up((size_t)gspn::large_bwd_state_floats(p.planes, (int)p.H) * 4, kWsAlign);
+}
+
 size_t fwd_ws_bytes(const Problem& p, int algo, uint32_t mask) {
+  if (saves_state(p, algo)) return saved_layout(p).total;
   if (algo == GSPN_ALGO_STREAM && p.n > 1 && !p.y_pd()) return round_up((size_t)p.npc * 4, kWsAlign);
   if (algo == GSPN_ALGO_TWO_PASS)
     return (p.y_pd() ? 0 : two_pass_acc_bytes(p, mask)) + two_pass_state_bytes(p, mask);
@@ -245,6 +282,7 @@ size_t gspn_scan_bwd_workspace_bytes(int64_t B, int64_t C, int64_t H, int64_t W,
   Problem p;
   if (check_shape(B, C, H, W, mask, dtype, group_h, group_w, flags, algo, &p) != GSPN_OK || p.empty)
     return 0;
+  if (saves_state(p, choose_algo(p, dtype, algo, false))) return saved_bwd_ws_bytes(p);
   const int a = choose_algo(p, dtype, algo, true);
   if (a < 0) return 0;
   // AUTO runs the streaming family instead of the resident one when a pointer
@@ -268,11 +306,13 @@ int gspn_scan_fwd(const void* x, const void* w, const void* lam, const void* u, 
   if (st != GSPN_OK) return st;
   int a = choose_algo(p, dtype, algo, false);
   if (a < 0) return GSPN_ERR_UNSUPPORTED;
+  const bool keep = saves_state(p, a);
   if (a == GSPN_ALGO_TWO_PASS) {
     // the two-pass kernels read and write 16-byte vectors
     for (const void* q : {x, w, lam, u, (const void*)y})
       if ((uintptr_t)q % 16) {
-        if (algo != GSPN_ALGO_AUTO) return GSPN_ERR_ALIGN;
+        // a kept state must come from the two-pass kernels: no fallback then
+        if (algo != GSPN_ALGO_AUTO || keep) return GSPN_ERR_ALIGN;
         a = GSPN_ALGO_STREAM;  // its workspace is never larger than the two-pass one
         break;
       }
@@ -300,6 +340,17 @@ int gspn_scan_fwd(const void* x, const void* w, const void* lam, const void* u, 
     l.acc_b = (!p.y_pd() && two_pass_split_v(mask))
                   ? (float*)((char*)workspace + round_up((size_t)p.npc * 4, kWsAlign)) : nullptr;
     l.state = (float*)((char*)workspace + accb);
+    if (keep) {
+      // vertical h in acc / acc_b, the sums and horizontal h in their arrays
+      const SavedLayout k = saved_layout(p);
+      auto at = [&](size_t off) { return off == kAbsent ? nullptr : (float*)((char*)workspace + off); };
+      l.acc = at(k.h[0] != kAbsent ? k.h[0] : k.h[1]);
+      l.acc_b = (k.h[0] != kAbsent && k.h[1] != kAbsent) ? at(k.h[1]) : nullptr;
+      l.sum = at(k.sum);
+      l.hsave[0] = at(k.h[2]);
+      l.hsave[1] = at(k.h[3]);
+      l.state = at(k.state);
+    }
     l.y_pd = p.y_pd();
     l.mask = mask; l.planes = p.planes; l.H = (int)H; l.W = (int)W; l.dtype = dtype;
     l.group_h = p.gh; l.group_w = p.gw;
@@ -339,6 +390,7 @@ int gspn_scan_fwd_noalloc(const void* x, const void* w, const void* lam, const v
   Problem p;
   int st = check_shape(B, C, H, W, mask, dtype, group_h, group_w, flags, GSPN_ALGO_AUTO, &p);
   if (st != GSPN_OK || p.empty) return st;
+  if (flags & GSPN_FLAG_SAVE_STATE) return GSPN_ERR_UNSUPPORTED;  // a kept state needs the caller's workspace
   const int a = choose_algo(p, dtype, GSPN_ALGO_AUTO, false);
   if (a < 0) return GSPN_ERR_UNSUPPORTED;
   // the AUTO size also covers the streaming fallback of misaligned two-pass calls
@@ -366,18 +418,21 @@ int gspn_scan_bwd(const void* dy, const void* x, const void* w, const void* lam,
   st = check_ptrs({{dy, yb}, {x, tb}, {w, wb}, {lam, lb}, {u, ub}},
                   {{dx, tb}, {dw, wb}, {dlam, lb}, {du, ub}}, es);
   if (st != GSPN_OK) return st;
-  int a = choose_algo(p, dtype, algo, true);
+  // a state kept by the forward (two-pass family) is read by the two-pass backward
+  bool keep = saves_state(p, choose_algo(p, dtype, algo, false));
+  int a = keep ? GSPN_ALGO_TWO_PASS : choose_algo(p, dtype, algo, true);
   if (a < 0) return GSPN_ERR_UNSUPPORTED;
   if (a == GSPN_ALGO_RESIDENT || a == GSPN_ALGO_RESIDENT_GENERIC || a == GSPN_ALGO_TWO_PASS) {
     // the resident and two-pass backward kernels read and write 16-byte vectors
     for (const void* q : {dy, x, w, lam, u, (const void*)dx, (const void*)dw, (const void*)dlam, (const void*)du})
       if ((uintptr_t)q % 16) {
         if (algo != GSPN_ALGO_AUTO) return GSPN_ERR_ALIGN;
-        a = GSPN_ALGO_STREAM;  // the AUTO workspace size includes this case
+        a = GSPN_ALGO_STREAM;  // the AUTO workspace size includes this case (a kept state is ignored)
+        keep = false;
         break;
       }
   }
-  const size_t need = bwd_ws_bytes(p, a);
+  const size_t need = keep ? saved_bwd_ws_bytes(p) : bwd_ws_bytes(p, a);
   st = check_ws(workspace, workspace_bytes, need,
                 {{dy, yb}, {x, tb}, {w, wb}, {lam, lb}, {u, ub}, {dx, tb}, {dw, wb}, {dlam, lb}, {du, ub}});
   if (st != GSPN_OK) return st;
@@ -402,9 +457,16 @@ int gspn_scan_bwd(const void* dy, const void* x, const void* w, const void* lam,
   if (a == GSPN_ALGO_TWO_PASS) {
     // horizontal directions first (their h through the first array), then the
     // vertical directions' h at once (first and fourth arrays), then their
-    // adjoints; the finish adds the vertical h to the horizontal sum
+    // adjoints; the finish adds the vertical h to the horizontal sum.  With a
+    // kept state every h and their sum come from the forward instead.
     float* hb = both_vertical(mask) ? (float*)((char*)workspace + 3 * fb) : nullptr;
     float* state = (float*)((char*)workspace + (both_vertical(mask) ? 4 : 3) * fb);
+    const SavedLayout k = saved_layout(p);
+    auto kept = [&](size_t off) { return off == kAbsent ? nullptr : (float*)((char*)workspace + off); };
+    if (keep) {
+      gsum = (float*)((char*)workspace + k.total);
+      state = (float*)((char*)workspace + k.total + fb);
+    }
     int slot[4] = {-1, -1, -1, -1};
     for (int i = 0; i < (int)ds.size(); ++i) slot[ds[i] == DIR_T2B ? 0 : ds[i] == DIR_B2T ? 1 : ds[i] == DIR_L2R ? 2 : 3] = i;
     bool first = true;
@@ -416,7 +478,8 @@ int gspn_scan_bwd(const void* dy, const void* x, const void* w, const void* lam,
       l.hdy = p.y_pd() ? l.dy : nullptr;
       l.w = (const char*)w + (size_t)slot[d] * 3 * tb;
       l.dw = (char*)dw + (size_t)slot[d] * 3 * tb;
-      l.hbuf = hprev; l.hsum = hsum; l.gsum = gsum; l.state = state;
+      l.hbuf = keep ? kept(k.h[d]) : hprev; l.hsum = keep ? nullptr : hsum; l.gsum = gsum; l.state = state;
+      l.saved = keep ? 1 : 0;
       l.first = first ? 1 : 0;
       l.dir = d == 3 ? 1 : 0;
       l.planes = p.planes; l.H = (int)H; l.W = (int)W;
@@ -428,7 +491,10 @@ int gspn_scan_bwd(const void* dy, const void* x, const void* w, const void* lam,
       first = false;
     }
     float* hv[2] = {nullptr, nullptr};  // h of top-to-bottom, bottom-to-top
-    if (slot[0] >= 0 || slot[1] >= 0) {
+    if (keep) {
+      hv[0] = kept(k.h[0]);
+      hv[1] = kept(k.h[1]);
+    } else if (slot[0] >= 0 || slot[1] >= 0) {
       hv[0] = slot[0] >= 0 ? hprev : nullptr;
       hv[1] = slot[1] >= 0 ? (slot[0] >= 0 ? hb : hprev) : nullptr;
       LargeBwdVArgs v{};
@@ -459,6 +525,11 @@ int gspn_scan_bwd(const void* dy, const void* x, const void* w, const void* lam,
     GradFinishArgs g{};
     g.x = x; g.lam = lam; g.dy = dy; g.gsum = gsum; g.hsum = hsum; g.hsum2 = hv[0] ? hv[0] : hv[1];
     g.hsum3 = hv[0] ? hv[1] : nullptr;
+    if (keep) {
+      // du = dy * sum_d h_d, the sum the forward formed
+      g.hsum = kept(k.sum);
+      g.hsum2 = g.hsum3 = nullptr;
+    }
     if (p.y_pd()) {
       // unmerged outputs: du = sum_d dy_d h_d (the horizontal part is in hsum)
       const int s2 = hv[0] ? slot[0] : slot[1], s3 = hv[0] ? slot[1] : -1;

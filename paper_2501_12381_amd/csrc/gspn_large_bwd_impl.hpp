@@ -348,7 +348,7 @@ hipError_t large_bwd_h_t(const LargeBwdHArgs& a) {
   h.hbuf = a.hbuf;
   h.renorm = a.renorm;
   h.hdy = a.hdy;
-  for (int j = 0; j < g.nblk; ++j) {
+  for (int j = 0; j < g.nblk && !a.saved; ++j) {
     const int blk = a.dir ? g.nblk - 1 - j : j;
     const int ws = window(blk);
     uint64_t m = 0;

@@ -364,6 +364,10 @@ struct LargeHParams {
   // rec mode with unmerged outputs: acc (+)= dy_d * h instead of h (dy_d: this
   // direction's output gradient), the sum du needs
   const void* hdy;
+  // forward keeping its state for the backward: the partial and final sums go
+  // to `sum` (acc keeps the vertical pass's h), each direction's h to hsave[dir]
+  float* sum;
+  float* hsave[2];
 };
 
 // LG: the weight maps hold Eq. 6 logits, normalised as they are unpacked.
@@ -450,6 +454,11 @@ __device__ __forceinline__ void large_h_body(const LargeHParams& p) {
   const bool add_b = p.acc_b != nullptr && !second && !p.y_pd;  // the vertical sum still lives in two arrays
   T* const yout = (T*)p.y + (p.y_pd ? (int64_t)slot * p.npc : 0);
   const T* const hdy = (const T*)p.hdy;
+  // the partial sum this launch adds to and where its result goes: acc, or
+  // with a kept state the separate sum array (acc keeps the vertical h)
+  const float* const acc_in = (second && p.sum) ? p.sum : p.acc;
+  float* const acc_out = p.sum ? p.sum : p.acc;
+  float* const hout = p.rec ? p.hbuf : p.hsave[dir];  // this direction's h, when kept
   const int rows = be - bs;
   const int nvr = (K - lo) / VE;
   const int n = rows * nvr;
@@ -461,7 +470,7 @@ __device__ __forceinline__ void large_h_body(const LargeHParams& p) {
     const int e = tid + k * TT < n ? tid + k * TT : 0;
     const int rr = e / nvr, cc = lo + (e - rr * nvr) * VE;
     const int64_t o = ob + (int64_t)rr * W + cc;
-    if (read_acc) ldv<VE>(p.acc + o, pav[k]);
+    if (read_acc) ldv<VE>(acc_in + o, pav[k]);
     if (add_b) ldv<VE>(p.acc_b + o, pbv[k]);
     if (fin) puv[k].load((const T*)p.u + o);
     if (hdy) puv[k].load(hdy + o);  // rec mode: the direction's dy (u is not needed there)
@@ -545,13 +554,14 @@ __device__ __forceinline__ void large_h_body(const LargeHParams& p) {
       const float hv = hdy ? lds[rr * KP + cc + q] * uv.get(q) : lds[rr * KP + cc + q];
       s[q] = (read_acc ? (add_b ? av[q] + bv[q] : av[q]) : 0.f) + hv;
     }
-    if (p.rec) stv<VE>(p.hbuf + o, lds + rr * KP + cc);
+    if (hout) stv<VE>(hout + o, lds + rr * KP + cc);
     if (fin) {
+      if (p.sum) stv<VE>(p.sum + o, s);  // sum_d h_d, kept for the backward
 #pragma unroll
       for (int q = 0; q < VE; ++q) s[q] *= uv.get(q);
       stv<VE>(yout + o, s);
     } else {
-      stv<VE>(p.acc + o, s);
+      stv<VE>(acc_out + o, s);
     }
   };
 #pragma unroll
@@ -566,7 +576,7 @@ __device__ __forceinline__ void large_h_body(const LargeHParams& p) {
       const int e = e0 + k * TT < n ? e0 + k * TT : e0;
       const int rr = e / nvr, cc = lo + (e - rr * nvr) * VE;
       const int64_t o = ob + (int64_t)rr * W + cc;
-      if (read_acc) ldv<VE>(p.acc + o, av[k]);
+      if (read_acc) ldv<VE>(acc_in + o, av[k]);
       if (add_b) ldv<VE>(p.acc_b + o, bv[k]);
       if (fin) uv[k].load((const T*)p.u + o);
       if (hdy) uv[k].load(hdy + o);
@@ -732,6 +742,9 @@ hipError_t large_fwd_t(const LargeFwdArgs& a) {
   h.renorm = a.renorm;
   h.y_pd = a.y_pd;
   h.acc_b = (slot[0] >= 0 && slot[1] >= 0 && a.acc_b != nullptr && !a.y_pd) ? a.acc_b : nullptr;
+  h.sum = a.y_pd ? nullptr : a.sum;
+  h.hsave[0] = a.y_pd ? nullptr : a.hsave[0];
+  h.hsave[1] = a.y_pd ? nullptr : a.hsave[1];
   const int64_t grid = (int64_t)g.hb_n * a.planes * (both ? 2 : 1);
   if (grid > 0x7fffffffLL) return hipErrorInvalidConfiguration;
   const int GW = (a.group_w > 0 && a.group_w < a.W) ? a.group_w : a.W;

@@ -156,6 +156,11 @@ struct LargeFwdArgs {
   int group_h, group_w;  // local-GSPN group lengths (0: global)
   int logits, renorm;    // w holds Eq. 6 logits (renorm: over on-line neighbours only)
   int y_pd;              // unmerged outputs (y is (n, B, C, H, W)); no partial sums needed
+  // state kept for the backward (null when not kept): acc / acc_b then keep
+  // the vertical directions' h, `sum` takes the horizontal pass's partial and
+  // final sums, hsave[0] / hsave[1] left-to-right's / right-to-left's h
+  float* sum;
+  float* hsave[2];
   void* stream;
 };
 hipError_t large_fwd_f32(const LargeFwdArgs& a);
@@ -184,6 +189,7 @@ struct LargeBwdHArgs {
   int group;         // columns per local-GSPN group (0 or >= W: global)
   int logits, renorm;  // w holds Eq. 6 logits; dw is the gradient for the logits
   const void* hdy;   // unmerged outputs: this direction's dy; hsum (+)= dy * h
+  int saved;         // hbuf already holds h (kept by the forward): no recompute, hsum untouched
   void* stream;
 };
 

@@ -17,7 +17,7 @@ GSPN_DIR_T2B, GSPN_DIR_B2T, GSPN_DIR_L2R, GSPN_DIR_R2L = 1, 2, 4, 8
 GSPN_ALGO_AUTO, GSPN_ALGO_RESIDENT, GSPN_ALGO_STREAM, GSPN_ALGO_RESIDENT_GENERIC = 0, 1, 2, 3
 GSPN_ALGO_TWO_PASS = 4
 GSPN_FLAG_W_LOGITS, GSPN_FLAG_EDGE_RENORM, GSPN_FLAG_LAM_PER_DIR = 1, 2, 4
-GSPN_FLAG_U_PER_DIR, GSPN_FLAG_Y_PER_DIR = 8, 16
+GSPN_FLAG_U_PER_DIR, GSPN_FLAG_Y_PER_DIR, GSPN_FLAG_SAVE_STATE = 8, 16, 32
 GSPN_MAX_LINE = 4096
 STATUS = {0: "GSPN_OK", 1: "GSPN_ERR_NULL", 2: "GSPN_ERR_SHAPE", 3: "GSPN_ERR_MASK",
           4: "GSPN_ERR_DTYPE", 5: "GSPN_ERR_ALIGN", 6: "GSPN_ERR_ALIAS",

@@ -10,7 +10,11 @@ Options (keyword arguments, all default off):
   logits, renorm   : w holds logits normalised by Eq. 6 inside the call
                      (renorm: over the on-line neighbours only);
   lam_per_dir, u_per_dir, y_per_dir : lam / u / y (and dy) stacked per
-                     direction, shape (n, B, C, H, W).
+                     direction, shape (n, B, C, H, W);
+  save_state       : the forward keeps its states in the workspace for the
+                     backward, which then does not recompute them (pass the
+                     same `workspace` tensor, from `scan_workspace`, to both
+                     calls; the two-pass kernels use it, others ignore it).
 """
 from __future__ import annotations
 
@@ -36,13 +40,15 @@ class ScanOptions:
     lam_per_dir: bool = False
     u_per_dir: bool = False
     y_per_dir: bool = False
+    save_state: bool = False
 
     @property
     def flags(self) -> int:
         return ((L.GSPN_FLAG_W_LOGITS if self.logits else 0) | (L.GSPN_FLAG_EDGE_RENORM if self.renorm else 0)
                 | (L.GSPN_FLAG_LAM_PER_DIR if self.lam_per_dir else 0)
                 | (L.GSPN_FLAG_U_PER_DIR if self.u_per_dir else 0)
-                | (L.GSPN_FLAG_Y_PER_DIR if self.y_per_dir else 0))
+                | (L.GSPN_FLAG_Y_PER_DIR if self.y_per_dir else 0)
+                | (L.GSPN_FLAG_SAVE_STATE if self.save_state else 0))
 
 
 def _dtype_code(t: torch.Tensor) -> int:
@@ -84,13 +90,28 @@ def _ptr(t):
     return t.data_ptr() if t is not None else None
 
 
+def scan_workspace(x, mask: int, *, algo: int = L.GSPN_ALGO_AUTO, group_h: int = 0, group_w: int = 0,
+                   **options) -> torch.Tensor:
+    """A workspace that serves a forward call and the backward call that
+    follows it (the backward's size covers the forward's; with save_state the
+    forward leaves its states at the start for the backward)."""
+    opt = ScanOptions(group_h, group_w, **options)
+    B, C, H, W = x.shape
+    dt = _dtype_code(x)
+    need = max(L.gspn_scan_fwd_workspace_bytes(B, C, H, W, mask, dt, group_h, group_w, opt.flags, algo),
+               L.gspn_scan_bwd_workspace_bytes(B, C, H, W, mask, dt, group_h, group_w, opt.flags, algo))
+    return torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
+
+
 def gspn_scan_fwd(x, w, lam, u, mask: int, *, algo: int = L.GSPN_ALGO_AUTO, y=None, workspace=None,
                   group_h: int = 0, group_w: int = 0, logits: bool = False, renorm: bool = False,
                   lam_per_dir: bool = False, u_per_dir: bool = False,
-                  y_per_dir: bool = False) -> torch.Tensor:
+                  y_per_dir: bool = False, save_state: bool = False) -> torch.Tensor:
     """y = u * sum_{d in mask} h_d (forward line scan of all directions in mask)."""
-    opt = ScanOptions(group_h, group_w, logits, renorm, lam_per_dir, u_per_dir, y_per_dir)
+    opt = ScanOptions(group_h, group_w, logits, renorm, lam_per_dir, u_per_dir, y_per_dir, save_state)
     _check(x, w, lam, u, mask, opt)
+    if save_state and workspace is None:
+        raise ValueError("save_state keeps the forward's states in `workspace`: pass one (scan_workspace)")
     x, w, lam, u = (t.contiguous() for t in (x, w, lam, u))
     B, C, H, W = x.shape
     dt = _dtype_code(x)
@@ -101,6 +122,8 @@ def gspn_scan_fwd(x, w, lam, u, mask: int, *, algo: int = L.GSPN_ALGO_AUTO, y=No
         raise ValueError(f"y must be a contiguous {x.dtype} tensor of shape {yshape}")
     need = L.gspn_scan_fwd_workspace_bytes(B, C, H, W, mask, dt, group_h, group_w, opt.flags, algo)
     if workspace is None or workspace.numel() < need:
+        if save_state:
+            raise ValueError(f"the workspace holds {workspace.numel()} bytes, the forward needs {need}")
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
     with torch.cuda.device(x.device):
         st = L.gspn_scan_fwd(_ptr(x), _ptr(w), _ptr(lam), _ptr(u), _ptr(y), B, C, H, W, mask, dt,
@@ -114,12 +137,16 @@ def gspn_scan_fwd(x, w, lam, u, mask: int, *, algo: int = L.GSPN_ALGO_AUTO, y=No
 def gspn_scan_bwd(dy, x, w, lam, u, mask: int, *, algo: int = L.GSPN_ALGO_AUTO, workspace=None,
                   out=None, group_h: int = 0, group_w: int = 0, logits: bool = False,
                   renorm: bool = False, lam_per_dir: bool = False, u_per_dir: bool = False,
-                  y_per_dir: bool = False):
+                  y_per_dir: bool = False, save_state: bool = False):
     """Gradients (dx, dw, dlam, du) of <dy, y> for the forward above.
 
-    `out` = (dx, dw, dlam, du): optional contiguous output tensors (else new ones)."""
-    opt = ScanOptions(group_h, group_w, logits, renorm, lam_per_dir, u_per_dir, y_per_dir)
+    `out` = (dx, dw, dlam, du): optional contiguous output tensors (else new ones).
+    save_state: `workspace` is the one the forward (called with save_state)
+    filled, unchanged since."""
+    opt = ScanOptions(group_h, group_w, logits, renorm, lam_per_dir, u_per_dir, y_per_dir, save_state)
     _check(x, w, lam, u, mask, opt)
+    if save_state and workspace is None:
+        raise ValueError("save_state reads the forward's states from `workspace`: pass the forward's")
     if dy.shape != _shape(x.shape, y_per_dir, n_dirs(mask)) or dy.dtype != x.dtype or dy.device != x.device:
         raise ValueError("dy must be shaped like y, typed and placed like x")
     dy, x, w, lam, u = (t.contiguous() for t in (dy, x, w, lam, u))
@@ -135,6 +162,8 @@ def gspn_scan_bwd(dy, x, w, lam, u, mask: int, *, algo: int = L.GSPN_ALGO_AUTO, 
                 raise ValueError("out tensors must be contiguous and shaped like (x, w, lam, u)")
     need = L.gspn_scan_bwd_workspace_bytes(B, C, H, W, mask, dt, group_h, group_w, opt.flags, algo)
     if workspace is None or workspace.numel() < need:
+        if save_state:
+            raise ValueError(f"the workspace holds {workspace.numel()} bytes, the backward needs {need}")
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
     with torch.cuda.device(x.device):
         st = L.gspn_scan_bwd(_ptr(dy), _ptr(x), _ptr(w), _ptr(lam), _ptr(u), _ptr(dx), _ptr(dw),
@@ -152,13 +181,16 @@ class GSPNScan(torch.autograd.Function):
     def forward(ctx, x, w, lam, u, mask: int, algo: int = L.GSPN_ALGO_AUTO, opt: ScanOptions = ScanOptions()):
         ctx.mask, ctx.algo, ctx.opt = mask, algo, opt
         ctx.save_for_backward(x, w, lam, u)
-        return gspn_scan_fwd(x, w, lam, u, mask, algo=algo, **opt.__dict__)
+        # with save_state the workspace carries the forward's states to the backward
+        ctx.ws = scan_workspace(x, mask, algo=algo, **opt.__dict__) if opt.save_state else None
+        return gspn_scan_fwd(x, w, lam, u, mask, algo=algo, workspace=ctx.ws, **opt.__dict__)
 
     @staticmethod
     def backward(ctx, dy):
         x, w, lam, u = ctx.saved_tensors
         dx, dw, dlam, du = gspn_scan_bwd(dy.contiguous(), x, w, lam, u, ctx.mask, algo=ctx.algo,
-                                         **ctx.opt.__dict__)
+                                         workspace=ctx.ws, **ctx.opt.__dict__)
+        ctx.ws = None
         return dx, dw, dlam, du, None, None, None
 
 

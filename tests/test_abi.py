@@ -46,7 +46,7 @@ def test_header_constants_match_binding():
                  "GSPN_DIR_R2L", "GSPN_ALGO_AUTO", "GSPN_ALGO_RESIDENT", "GSPN_ALGO_STREAM",
                  "GSPN_ALGO_RESIDENT_GENERIC", "GSPN_ALGO_TWO_PASS", "GSPN_FLAG_W_LOGITS",
                  "GSPN_FLAG_EDGE_RENORM", "GSPN_FLAG_LAM_PER_DIR", "GSPN_FLAG_U_PER_DIR",
-                 "GSPN_FLAG_Y_PER_DIR"):
+                 "GSPN_FLAG_Y_PER_DIR", "GSPN_FLAG_SAVE_STATE"):
         assert int(consts[name]) == getattr(L, name), name
     for code, name in L.STATUS.items():
         assert int(consts[name]) == code, name
@@ -150,7 +150,7 @@ def test_fwd_rejects_bad_arguments(lib):
     # the two-pass kernels need 16-byte aligned tensors when forced
     assert fwd(algo=L.GSPN_ALGO_TWO_PASS, W=64, dtype=L.GSPN_BF16, x=FAKE + 2) == 5
     # options: unknown flags, edge renormalisation without logits, negative groups
-    assert fwd(flags=32) == 7
+    assert fwd(flags=64) == 7
     assert fwd(flags=L.GSPN_FLAG_EDGE_RENORM) == 7
     assert fwd(group_h=-1) == 7
     assert fwd(group_w=-2) == 7
@@ -231,3 +231,56 @@ def test_workspace_sizes_with_options():
     # invalid options report 0
     assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 7, 0xF, f32, flags=1 << 7, algo=A) == 0
     assert L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 7, 0xF, f32, group_h=-1, algo=A) == 0
+
+
+def test_workspace_sizes_with_saved_state():
+    """GSPN_FLAG_SAVE_STATE on the two-pass family: the forward keeps the
+    present directions' h and sum_d h_d (fp32 arrays) and its column state; the
+    backward's size is that plus the sum of g and the adjoint's column products.
+    Problems the flag does not apply to keep their sizes."""
+    bf, T, A = L.GSPN_BF16, L.GSPN_ALGO_TWO_PASS, L.GSPN_ALGO_AUTO
+    K = L.GSPN_FLAG_SAVE_STATE
+    fb, state, bstate = 2 * 3 * 5 * 64 * 4, 512, 768
+    fwd_ws = lambda mask, flags=K, algo=T, **kw: L.gspn_scan_fwd_workspace_bytes(2, 3, 5, 64, mask, bf, flags=flags,
+                                                                                 algo=algo, **kw)
+    bwd_ws = lambda mask, flags=K, algo=T: L.gspn_scan_bwd_workspace_bytes(2, 3, 5, 64, mask, bf, flags=flags,
+                                                                           algo=algo)
+    # h of T2B, B2T, the sum, h of L2R, R2L, then the column state
+    assert fwd_ws(0xF) == 5 * fb + state
+    assert fwd_ws(0x4) == 2 * fb + state
+    assert fwd_ws(0x5) == 3 * fb + state
+    assert fwd_ws(0xE) == 4 * fb + state
+    assert fwd_ws(0xF, flags=K | L.GSPN_FLAG_W_LOGITS, group_w=7) == 5 * fb + state
+    for m in (0xF, 0x4, 0x5, 0xE, 0x9):
+        assert bwd_ws(m) == fwd_ws(m) + fb + bstate
+    # no horizontal direction, or unmerged outputs: the flag changes nothing
+    assert fwd_ws(0x3) == fwd_ws(0x3, flags=0)
+    assert bwd_ws(0x3) == bwd_ws(0x3, flags=0) == 0
+    Y = L.GSPN_FLAG_Y_PER_DIR
+    assert fwd_ws(0xF, flags=K | Y) == fwd_ws(0xF, flags=Y)
+    assert bwd_ws(0xF, flags=K | Y) == bwd_ws(0xF, flags=Y)
+    # AUTO: the two-pass family for large planes, the flag ignored where a
+    # plane stays on chip
+    big = 2 * 2048 * 2048 * 4
+    assert L.gspn_scan_fwd_workspace_bytes(1, 2, 2048, 2048, 0xF, bf, flags=K, algo=A) == 5 * big + 4 * 2 * 2048 * 4
+    assert (L.gspn_scan_bwd_workspace_bytes(1, 2, 2048, 2048, 0xF, bf, flags=K, algo=A)
+            == 6 * big + 4 * 2 * 2048 * 4 + 6 * 2 * 2048 * 4)
+    for S in (28, 128):
+        assert (L.gspn_scan_fwd_workspace_bytes(4, 8, S, S, 0xF, bf, flags=K, algo=A)
+                == L.gspn_scan_fwd_workspace_bytes(4, 8, S, S, 0xF, bf, algo=A))
+        assert (L.gspn_scan_bwd_workspace_bytes(4, 8, S, S, 0xF, bf, flags=K, algo=A)
+                == L.gspn_scan_bwd_workspace_bytes(4, 8, S, S, 0xF, bf, algo=A))
+
+
+def test_saved_state_refusals(lib):
+    """A kept state must come from the two-pass kernels: the forward refuses
+    element-aligned tensors instead of falling back to streaming, and the
+    allocation-free forward refuses the flag (fake pointers, rejected before
+    any launch)."""
+    _no_gpu()
+    K = L.GSPN_FLAG_SAVE_STATE
+    big = dict(H=2048, W=64, dtype=L.GSPN_BF16, ws_bytes=1 << 30)
+    assert fwd(algo=L.GSPN_ALGO_AUTO, flags=K, x=FAKE + 2, **big) == 5
+    assert fwd(algo=L.GSPN_ALGO_TWO_PASS, flags=K, u=FAKE + (3 << 30) + 8, **big) == 5
+    assert L.gspn_scan_fwd_noalloc(FAKE, FAKE + (1 << 30), FAKE + (2 << 30), FAKE + (3 << 30), FAKE + (4 << 30),
+                                   1, 2, 8, 64, 0xF, L.GSPN_BF16, 0, 0, K, None) == 7
