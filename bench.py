@@ -3,8 +3,10 @@
 
 One step = one pass of the whole hot path over one batch of synthetic input:
 the forward scan and, for workloads with a backward, the adjoint scan that
-produces dx, dw, dlam and du.  Inputs are generated on the device (seeded)
-before the timed region; nothing is copied over PCIe inside it.
+produces dx, dw, dlam and du (as in training, the forward keeps its states in
+the workspace for the backward where the kernel family supports it).  Inputs
+are generated on the device (seeded) before the timed region; nothing is
+copied over PCIe inside it.
 
 The headline line measures the largest single-GPU workload: the 4-direction
 bf16 forward on 1 x 320 x 2048 x 2048 planes (an image latent of about 16K
@@ -164,15 +166,21 @@ def measure(wl, algo: int, bwd_algo: int, steps: int, warmup: int, cold_reps: in
     torch.cuda.synchronize()
     x, w, lam, u = inp["x"], inp["w"], inp["lam"], inp["u"]
     y = torch.empty_like(x)
+    # a training step keeps the forward's states for the backward (the kernel
+    # families that keep a plane on chip ignore the option); one workspace
+    # serves both calls
+    save = wl.backward and algo == bwd_algo
+    ws = ops.scan_workspace(x, wl.mask, algo=algo, save_state=True, logits=wl.logits) if save else None
 
     def step(ev=None):
         if ev is not None:
             ev[0].record()
-        ops.gspn_scan_fwd(x, w, lam, u, wl.mask, algo=algo, y=y, logits=wl.logits)
+        ops.gspn_scan_fwd(x, w, lam, u, wl.mask, algo=algo, y=y, logits=wl.logits, workspace=ws, save_state=save)
         if ev is not None:
             ev[1].record()
         if wl.backward:
-            ops.gspn_scan_bwd(inp["dy"], x, w, lam, u, wl.mask, algo=bwd_algo, logits=wl.logits)
+            ops.gspn_scan_bwd(inp["dy"], x, w, lam, u, wl.mask, algo=bwd_algo, logits=wl.logits, workspace=ws,
+                              save_state=save)
             if ev is not None:
                 ev[2].record()
 
@@ -225,7 +233,7 @@ def measure(wl, algo: int, bwd_algo: int, steps: int, warmup: int, cold_reps: in
                 "bwd_frac": alg_bytes(wl, "bwd") / (c_bwd / 1e3) / (HBM_PEAK_GBS * 1e9)
                 if wl.backward else None,
                 "step_us": (c_fwd + c_bwd) * 1e3}
-    del inp, x, w, lam, u, y
+    del inp, x, w, lam, u, y, ws
     torch.cuda.empty_cache()
 
     dom = "bwd" if wl.backward and bwd_ms > fwd_ms else "fwd"
@@ -233,6 +241,7 @@ def measure(wl, algo: int, bwd_algo: int, steps: int, warmup: int, cold_reps: in
     r = {"workload": wl.name, "B": wl.B, "C": wl.C, "H": wl.H, "W": wl.W, "mask": wl.mask,
          "directions": wl.n_dirs, "dtype": wl.dtype, "pass": "fwd+bwd" if wl.backward else "fwd",
          "weights": "eq6_logits" if wl.logits else "normalised",
+         "forward_state": "kept for the backward" if save else None,
          "ms_per_step": ms_step, "value": wl.B * wl.C * wl.H * wl.W * wl.n_dirs / (ms_step / 1e3),
          "step_alg_bytes": step_bytes,
          "step_roofline_frac": step_bytes / (ms_step / 1e3) / (HBM_PEAK_GBS * 1e9),

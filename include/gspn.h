@@ -157,6 +157,10 @@ enum {
                             Unmerged outputs (GSPN_FLAG_Y_PER_DIR): the forward
                             writes each direction's y and needs only the column
                             state; the backward seeds each direction from its dy.
+                            GSPN_FLAG_SAVE_STATE: the forward keeps every h and
+                            the sum (one fp32 array per direction, one for the
+                            sum, and the column state), the backward runs only
+                            the adjoints on them (see the flag).
                             Needs W * element size a multiple of 16 bytes and at
                             least 128 bytes, W <= 4096 (bf16) or 2048 (f32), and
                             16-byte aligned tensors (AUTO falls back to streaming). */
