@@ -171,6 +171,13 @@ def measure(wl, algo: int, bwd_algo: int, steps: int, warmup: int, cold_reps: in
     # serves both calls
     save = wl.backward and algo == bwd_algo
     ws = ops.scan_workspace(x, wl.mask, algo=algo, save_state=True, logits=wl.logits) if save else None
+    kept = None
+    if save:
+        from paper_2501_12381_amd import lib as L
+        sizes = [L.gspn_scan_fwd_workspace_bytes(wl.B, wl.C, wl.H, wl.W, wl.mask, ops._dtype_code(x),
+                                                 flags=f | (L.GSPN_FLAG_W_LOGITS if wl.logits else 0), algo=algo)
+                 for f in (0, L.GSPN_FLAG_SAVE_STATE)]
+        kept = "kept for the backward" if sizes[1] > sizes[0] else "recomputed by the backward (on chip)"
 
     def step(ev=None):
         if ev is not None:
@@ -241,7 +248,7 @@ def measure(wl, algo: int, bwd_algo: int, steps: int, warmup: int, cold_reps: in
     r = {"workload": wl.name, "B": wl.B, "C": wl.C, "H": wl.H, "W": wl.W, "mask": wl.mask,
          "directions": wl.n_dirs, "dtype": wl.dtype, "pass": "fwd+bwd" if wl.backward else "fwd",
          "weights": "eq6_logits" if wl.logits else "normalised",
-         "forward_state": "kept for the backward" if save else None,
+         "forward_state": kept,
          "ms_per_step": ms_step, "value": wl.B * wl.C * wl.H * wl.W * wl.n_dirs / (ms_step / 1e3),
          "step_alg_bytes": step_bytes,
          "step_roofline_frac": step_bytes / (ms_step / 1e3) / (HBM_PEAK_GBS * 1e9),
