@@ -230,10 +230,12 @@ SavedLayout saved_layout(const Problem& p) {
   return l;
 }
 // backward reading the kept state: the forward's bytes, the sum of g, the
-// adjoint's column products
+// column products of the two horizontal adjoints (they run together)
+size_t bwd_state_bytes(const Problem& p) {
+  return round_up((size_t)gspn::large_bwd_state_floats(p.planes, (int)p.H) * 4, kWsAlign);
+}
 size_t saved_bwd_ws_bytes(const Problem& p) {
-  return saved_layout(p).total + round_up((size_t)p.npc * 4, kWsAlign) +
-         round_up((size_t)gspn::large_bwd_state_floats(p.planes, (int)p.H) * 4, kWsAlign);
+  return saved_layout(p).total + round_up((size_t)p.npc * 4, kWsAlign) + 2 * bwd_state_bytes(p);
 }
 
 size_t fwd_ws_bytes(const Problem& p, int algo, uint32_t mask) {
@@ -470,9 +472,10 @@ int gspn_scan_bwd(const void* dy, const void* x, const void* w, const void* lam,
     int slot[4] = {-1, -1, -1, -1};
     for (int i = 0; i < (int)ds.size(); ++i) slot[ds[i] == DIR_T2B ? 0 : ds[i] == DIR_B2T ? 1 : ds[i] == DIR_L2R ? 2 : 3] = i;
     bool first = true;
+    LargeBwdHArgs hz[2] = {};
     for (int d = 2; d < 4; ++d) {
       if (slot[d] < 0) continue;
-      LargeBwdHArgs l{};
+      LargeBwdHArgs& l = hz[d - 2];
       l.x = x; l.lam = lam; l.u = u;
       l.dy = (const char*)dy + (p.y_pd() ? (size_t)slot[d] * tb : 0);
       l.hdy = p.y_pd() ? l.dy : nullptr;
@@ -486,9 +489,18 @@ int gspn_scan_bwd(const void* dy, const void* x, const void* w, const void* lam,
       l.group = p.gw;
       l.logits = p.logits(); l.renorm = (flags & GSPN_FLAG_EDGE_RENORM) ? 1 : 0;
       l.stream = stream;
+      if (keep && slot[2] >= 0 && slot[3] >= 0) {
+        // both adjoints at once below, each with its own column products
+        if (d == 3) l.state = (float*)((char*)state + bwd_state_bytes(p));
+        continue;
+      }
       st = hip_status(large_bwd_h(l, dtype));
       if (st != GSPN_OK) return st;
       first = false;
+    }
+    if (keep && slot[2] >= 0 && slot[3] >= 0) {
+      st = hip_status(large_bwd_h_pair(hz[0], hz[1], dtype));
+      if (st != GSPN_OK) return st;
     }
     float* hv[2] = {nullptr, nullptr};  // h of top-to-bottom, bottom-to-top
     if (keep) {

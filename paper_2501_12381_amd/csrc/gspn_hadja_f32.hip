@@ -10,4 +10,12 @@ template hipError_t launch_large_hadj_nw<float, 3>(const LargeHAdjParams& p, int
                                                   hipStream_t st);
 template hipError_t launch_large_hadj_nw<float, 4>(const LargeHAdjParams& p, int dir, int64_t grid, size_t lds, bool lg,
                                                   hipStream_t st);
+template hipError_t launch_large_hadj2_nw<float, 1>(const LargeHAdjParams& p0, const LargeHAdjParams& p1,
+                                                   int64_t grid, size_t lds, bool lg, hipStream_t st);
+template hipError_t launch_large_hadj2_nw<float, 2>(const LargeHAdjParams& p0, const LargeHAdjParams& p1,
+                                                   int64_t grid, size_t lds, bool lg, hipStream_t st);
+template hipError_t launch_large_hadj2_nw<float, 3>(const LargeHAdjParams& p0, const LargeHAdjParams& p1,
+                                                   int64_t grid, size_t lds, bool lg, hipStream_t st);
+template hipError_t launch_large_hadj2_nw<float, 4>(const LargeHAdjParams& p0, const LargeHAdjParams& p1,
+                                                   int64_t grid, size_t lds, bool lg, hipStream_t st);
 }  // namespace gspn

@@ -4,4 +4,6 @@
 namespace gspn {
 template hipError_t launch_large_hadj_nw<bf16, 8>(const LargeHAdjParams& p, int dir, int64_t grid, size_t lds, bool lg,
                                                   hipStream_t st);
+template hipError_t launch_large_hadj2_nw<bf16, 8>(const LargeHAdjParams& p0, const LargeHAdjParams& p1,
+                                                   int64_t grid, size_t lds, bool lg, hipStream_t st);
 }  // namespace gspn

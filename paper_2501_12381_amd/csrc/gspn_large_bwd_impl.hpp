@@ -60,8 +60,9 @@ struct LargeHAdjParams {
 // DIR 0: left-to-right (its adjoint walks the blocks and columns right to left);
 // DIR 1: right-to-left (adjoint left to right).  LG: the weight maps hold
 // Eq. 6 logits; dw becomes their gradient.
+// b / G: the workgroup's index among the G workgroups of this direction.
 template <typename T, int NW, int DIR, bool LG>
-__global__ void __launch_bounds__(64 * NW) large_hadj_kernel(LargeHAdjParams p) {
+__device__ __forceinline__ void large_hadj_body(const LargeHAdjParams& p, int64_t b, int64_t G) {
   using C = LargeCfg<T>;
   constexpr int K = C::KH, HV = C::HV, VE = C::VE;
   constexpr int HC = K + 4;           // h columns in LDS: the window and 4 on its scan-previous side
@@ -75,8 +76,8 @@ __global__ void __launch_bounds__(64 * NW) large_hadj_kernel(LargeHAdjParams p) 
   float* edge = lds + (p.edge_rows + 2) * HP;
   constexpr int ES = (NW + 2) * 2;
 
+  if (p.step < 0 || p.step >= p.nblk) return;  // this direction has no block in the launch
   // workgroup -> (plane, band); the bands of a plane share an XCD
-  const int64_t G = gridDim.x, b = blockIdx.x;
   const int64_t G8 = G / 8 * 8;
   const int64_t id = b < G8 ? (b % 8) * (G8 / 8) + b / 8 : b;
   const int band = (int)(id % p.nbands);
@@ -282,9 +283,53 @@ __global__ void __launch_bounds__(64 * NW) large_hadj_kernel(LargeHAdjParams p) 
   }
 }
 
+template <typename T, int NW, int DIR, bool LG>
+__global__ void __launch_bounds__(64 * NW) large_hadj_kernel(LargeHAdjParams p) {
+  large_hadj_body<T, NW, DIR, LG>(p, blockIdx.x, gridDim.x);
+}
+// Both horizontal adjoints in one grid (each direction's h kept by the
+// forward, so neither waits for the other's recompute): the first half of
+// the workgroups runs left-to-right's adjoint, the second half
+// right-to-left's, each on its own column block of the launch.
+template <typename T, int NW, bool LG>
+__global__ void __launch_bounds__(64 * NW) large_hadj2_kernel(LargeHAdjParams p0, LargeHAdjParams p1) {
+  const int64_t half = gridDim.x / 2, b = blockIdx.x;
+  if (b < half) large_hadj_body<T, NW, 0, LG>(p0, b, half);
+  else large_hadj_body<T, NW, 1, LG>(p1, b - half, half);
+}
+
 // ---------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------
+
+// grid: workgroups per direction
+template <typename T, int NW>
+hipError_t launch_large_hadj2_nw(const LargeHAdjParams& p0, const LargeHAdjParams& p1, int64_t grid, size_t lds,
+                                 bool lg, hipStream_t st) {
+  auto kern = lg ? large_hadj2_kernel<T, NW, true> : large_hadj2_kernel<T, NW, false>;
+  if (lds > 64 * 1024) {
+    hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(kern, dim3((unsigned)(2 * grid)), dim3(64 * NW), lds, st, p0, p1);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_large_hadj2(const LargeHAdjParams& p0, const LargeHAdjParams& p1, int nw, int64_t grid,
+                              size_t lds, bool lg, hipStream_t st) {
+  switch (nw) {
+    case 1: return launch_large_hadj2_nw<T, 1>(p0, p1, grid, lds, lg, st);
+    case 2: return launch_large_hadj2_nw<T, 2>(p0, p1, grid, lds, lg, st);
+    case 3: return launch_large_hadj2_nw<T, 3>(p0, p1, grid, lds, lg, st);
+    case 4: return launch_large_hadj2_nw<T, 4>(p0, p1, grid, lds, lg, st);
+    case 5: return launch_large_hadj2_nw<T, 5>(p0, p1, grid, lds, lg, st);
+    case 6: return launch_large_hadj2_nw<T, 6>(p0, p1, grid, lds, lg, st);
+    case 7: return launch_large_hadj2_nw<T, 7>(p0, p1, grid, lds, lg, st);
+    case 8: return launch_large_hadj2_nw<T, 8>(p0, p1, grid, lds, lg, st);
+    default: return hipErrorInvalidValue;
+  }
+}
 
 template <typename T, int NW>
 hipError_t launch_large_hadj_nw(const LargeHAdjParams& p, int dir, int64_t grid, size_t lds, bool lg,
@@ -312,6 +357,44 @@ hipError_t launch_large_hadj(const LargeHAdjParams& p, int dir, int nw, int64_t 
     case 7: return launch_large_hadj_nw<T, 7>(p, dir, grid, lds, lg, st);
     case 8: return launch_large_hadj_nw<T, 8>(p, dir, grid, lds, lg, st);
     default: return hipErrorInvalidValue;
+  }
+}
+
+// parameters of the banded adjoint of one horizontal direction, and its
+// per-launch block (step j of the adjoint's order; outside [0, nblk) the
+// direction has nothing to do in the launch) with that block's group masks
+template <typename T>
+LargeHAdjParams large_hadj_params(const LargeBwdHArgs& a, const LargeGeom<T>& g) {
+  LargeHAdjParams p{};
+  p.dy = a.dy; p.u = a.u; p.w = a.w; p.dw = a.dw; p.hbuf = a.hbuf; p.gsum = a.gsum; p.state = a.state;
+  p.planes = a.planes; p.npc = a.planes * (int64_t)a.H * a.W; p.H = a.H; p.W = a.W;
+  p.first = a.first;
+  p.renorm = a.renorm;
+  p.nblk = g.nblk;
+  p.band_rows = g.hb_mid; p.edge_rows = g.hb_edge; p.nbands = g.hb_n; p.halo = g.halo;
+  return p;
+}
+template <typename T>
+size_t large_hadj_lds(const LargeGeom<T>& g) {
+  return ((size_t)(g.hb_edge + 2) * (LargeCfg<T>::KH + 5) + 4 * (8 + 2) + 64) * sizeof(float);
+}
+template <typename T>
+void large_hadj_step(LargeHAdjParams& p, const LargeBwdHArgs& a, const LargeGeom<T>& g, int j) {
+  constexpr int K = LargeCfg<T>::KH;
+  p.step = j;
+  p.zmask = p.gmask = 0;
+  if (j < 0 || j >= g.nblk) return;
+  const int GW = (a.group > 0 && a.group < a.W) ? a.group : a.W;
+  if (GW >= a.W) return;
+  // scan order: left-to-right visits column c after c - 1, right-to-left after c + 1
+  auto starts = [&](int c) { return a.dir ? ((c + 1) % GW == 0) : (c % GW == 0); };
+  const int blk = a.dir ? j : g.nblk - 1 - j;
+  const int c0 = blk * K;
+  const int ws = c0 + K <= a.W ? c0 : a.W - K;
+  for (int i = 0; i < K; ++i) {
+    const int c = ws + i, nxt = a.dir ? c - 1 : c + 1;
+    if (starts(c)) p.gmask |= 1ull << i;
+    if (nxt >= 0 && nxt < a.W && starts(nxt)) p.zmask |= 1ull << i;
   }
 }
 
@@ -363,28 +446,38 @@ hipError_t large_bwd_h_t(const LargeBwdHArgs& a) {
   }
 
   // adjoint: blocks in reverse scan order
-  LargeHAdjParams p{};
-  p.dy = a.dy; p.u = a.u; p.w = a.w; p.dw = a.dw; p.hbuf = a.hbuf; p.gsum = a.gsum; p.state = a.state;
-  p.planes = a.planes; p.npc = npc; p.H = a.H; p.W = a.W;
-  p.first = a.first;
-  p.renorm = a.renorm;
-  p.nblk = g.nblk;
-  p.band_rows = g.hb_mid; p.edge_rows = g.hb_edge; p.nbands = g.hb_n; p.halo = g.halo;
-  const size_t lds = ((size_t)(g.hb_edge + 2) * (K + 5) + 4 * (8 + 2) + 64) * sizeof(float);
+  LargeHAdjParams p = large_hadj_params<T>(a, g);
   for (int j = 0; j < g.nblk; ++j) {
-    const int blk = a.dir ? j : g.nblk - 1 - j;
-    const int ws = window(blk);
-    uint64_t zm = 0, gm = 0;
-    if (GW < a.W)
-      for (int i = 0; i < K; ++i) {
-        const int c = ws + i, nxt = a.dir ? c - 1 : c + 1;
-        if (starts(c)) gm |= 1ull << i;
-        if (nxt >= 0 && nxt < a.W && starts(nxt)) zm |= 1ull << i;
-      }
-    p.step = j;
-    p.zmask = zm;
-    p.gmask = gm;
-    hipError_t e = launch_large_hadj<T>(p, a.dir, g.hb_nw, grid, lds, a.logits != 0, st);
+    large_hadj_step(p, a, g, j);
+    hipError_t e = launch_large_hadj<T>(p, a.dir, g.hb_nw, grid, large_hadj_lds<T>(g), a.logits != 0, st);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+// Both horizontal adjoints at once on h kept by the forward (l2r.saved and
+// r2l.saved): one launch per column block, left-to-right's adjoint on block
+// nblk - 1 - j, right-to-left's on block j (one launch later for an odd block
+// count, so no block is visited by both in one launch).  The direction that
+// reaches a block first stores its g in gsum, the other adds: every element
+// gets the same two terms as in the sequential order (addition of two terms
+// commutes exactly).  Each direction has its own column-product state.
+template <typename T>
+hipError_t large_bwd_h_pair_t(const LargeBwdHArgs& l2r, const LargeBwdHArgs& r2l) {
+  if (!large_fwd_supported<T>(l2r.H, l2r.W)) return hipErrorInvalidValue;
+  if (!l2r.saved || !r2l.saved || l2r.dir != 0 || r2l.dir != 1) return hipErrorInvalidValue;
+  const LargeGeom<T> g = large_geom<T>(l2r.H, l2r.W);
+  const int64_t grid = (int64_t)g.hb_n * l2r.planes;
+  if (2 * grid > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+  LargeHAdjParams p0 = large_hadj_params<T>(l2r, g), p1 = large_hadj_params<T>(r2l, g);
+  const int delay = g.nblk & 1;
+  for (int j = 0; j < g.nblk + delay; ++j) {
+    const bool first = 2 * j < g.nblk - 1 + delay;  // both directions reach their blocks first
+    large_hadj_step(p0, l2r, g, j);
+    large_hadj_step(p1, r2l, g, j - delay);
+    p0.first = p1.first = first ? 1 : 0;
+    hipError_t e = launch_large_hadj2<T>(p0, p1, g.hb_nw, grid, large_hadj_lds<T>(g), l2r.logits != 0,
+                                         (hipStream_t)l2r.stream);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;

@@ -243,5 +243,12 @@ hipError_t large_bwd_h_bf16(const LargeBwdHArgs& a);
 inline hipError_t large_bwd_h(const LargeBwdHArgs& a, int dtype) {
   return dtype == 0 ? large_bwd_h_f32(a) : large_bwd_h_bf16(a);
 }
+// both horizontal directions' adjoints at once, on h kept by the forward
+// (l2r: dir 0, r2l: dir 1, both with saved set; separate state arrays)
+hipError_t large_bwd_h_pair_f32(const LargeBwdHArgs& l2r, const LargeBwdHArgs& r2l);
+hipError_t large_bwd_h_pair_bf16(const LargeBwdHArgs& l2r, const LargeBwdHArgs& r2l);
+inline hipError_t large_bwd_h_pair(const LargeBwdHArgs& l2r, const LargeBwdHArgs& r2l, int dtype) {
+  return dtype == 0 ? large_bwd_h_pair_f32(l2r, r2l) : large_bwd_h_pair_bf16(l2r, r2l);
+}
 
 }  // namespace gspn

@@ -236,8 +236,8 @@ def test_workspace_sizes_with_options():
 def test_workspace_sizes_with_saved_state():
     """GSPN_FLAG_SAVE_STATE on the two-pass family: the forward keeps the
     present directions' h and sum_d h_d (fp32 arrays) and its column state; the
-    backward's size is that plus the sum of g and the adjoint's column products.
-    Problems the flag does not apply to keep their sizes."""
+    backward's size is that plus the sum of g and the column products of the two
+    horizontal adjoints.  Problems the flag does not apply to keep their sizes."""
     bf, T, A = L.GSPN_BF16, L.GSPN_ALGO_TWO_PASS, L.GSPN_ALGO_AUTO
     K = L.GSPN_FLAG_SAVE_STATE
     fb, state, bstate = 2 * 3 * 5 * 64 * 4, 512, 768
@@ -252,7 +252,7 @@ def test_workspace_sizes_with_saved_state():
     assert fwd_ws(0xE) == 4 * fb + state
     assert fwd_ws(0xF, flags=K | L.GSPN_FLAG_W_LOGITS, group_w=7) == 5 * fb + state
     for m in (0xF, 0x4, 0x5, 0xE, 0x9):
-        assert bwd_ws(m) == fwd_ws(m) + fb + bstate
+        assert bwd_ws(m) == fwd_ws(m) + fb + 2 * bstate  # one column-product state per horizontal adjoint
     # no horizontal direction, or unmerged outputs: the flag changes nothing
     assert fwd_ws(0x3) == fwd_ws(0x3, flags=0)
     assert bwd_ws(0x3) == bwd_ws(0x3, flags=0) == 0
@@ -264,7 +264,7 @@ def test_workspace_sizes_with_saved_state():
     big = 2 * 2048 * 2048 * 4
     assert L.gspn_scan_fwd_workspace_bytes(1, 2, 2048, 2048, 0xF, bf, flags=K, algo=A) == 5 * big + 4 * 2 * 2048 * 4
     assert (L.gspn_scan_bwd_workspace_bytes(1, 2, 2048, 2048, 0xF, bf, flags=K, algo=A)
-            == 6 * big + 4 * 2 * 2048 * 4 + 6 * 2 * 2048 * 4)
+            == 6 * big + 4 * 2 * 2048 * 4 + 2 * 6 * 2 * 2048 * 4)
     for S in (28, 128):
         assert (L.gspn_scan_fwd_workspace_bytes(4, 8, S, S, 0xF, bf, flags=K, algo=A)
                 == L.gspn_scan_fwd_workspace_bytes(4, 8, S, S, 0xF, bf, algo=A))
